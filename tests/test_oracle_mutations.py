@@ -1,0 +1,133 @@
+"""Planted mistakes in the oracle (CPU only): each plausible error in the
+oracle's arithmetic must make at least one of the pins fail.  The mistakes
+are planted in copies of the oracle's functions via monkeypatch, never in the
+GPU path."""
+
+from math import factorial, sqrt
+
+import numpy as np
+import pytest
+
+import oracle.cg as ocg
+import oracle.conv as oconv
+from oracle.sh import block_diag_D, random_rotation, wigner_D_real
+
+
+@pytest.fixture(autouse=True)
+def _fresh_caches():
+    for fn in (ocg.cg_complex, ocg._U, ocg._real_block, ocg._dense_R):
+        fn.cache_clear()
+    yield
+    for fn in (ocg.cg_complex, ocg._U, ocg._real_block, ocg._dense_R):
+        fn.cache_clear()
+
+
+def _cross_relation_holds():
+    R = ocg._real_block(1, 1, 1)
+    rng = np.random.default_rng(3)
+    a, b = rng.normal(size=3), rng.normal(size=3)
+    u = np.einsum("abc,b,c->a", R, a[[1, 2, 0]], b[[1, 2, 0]])
+    return np.abs(u[[2, 0, 1]] - np.cross(a, b) / sqrt(2)).max() < 1e-12
+
+
+def _equivariant(L=3):
+    rng = np.random.default_rng(9)
+    g = random_rotation(rng)
+    D = block_diag_D(wigner_D_real(L, g, rng))
+    R = ocg._dense_R(L)
+    lhs = np.einsum("abc,bx,cy->axy", R, D, D)
+    rhs = np.einsum("ab,bxy->axy", D, R)
+    return np.abs(lhs - rhs).max() < 1e-10
+
+
+def _orthogonal(l1=2, l2=1):
+    rows = [ocg.complex_cg_block(l1, l2, J).reshape(2 * J + 1, -1)
+            for J in range(abs(l1 - l2), l1 + l2 + 1)]
+    C = np.concatenate(rows)
+    return np.abs(C @ C.T - np.eye(C.shape[0])).max() < 1e-12
+
+
+def test_baseline_pins_hold():
+    assert _cross_relation_holds() and _equivariant() and _orthogonal()
+
+
+def test_dropped_alternating_sign_is_caught(monkeypatch):
+    orig = ocg.cg_complex.__wrapped__
+
+    def bad(l1, m1, l2, m2, J, M):
+        v = orig(l1, m1, l2, m2, J, M)
+        # plant: drop (-1)^t by taking |.| of every coefficient
+        return abs(v)
+    monkeypatch.setattr(ocg, "cg_complex", bad)
+    assert not _orthogonal()
+
+
+def test_wrong_U_phase_is_caught(monkeypatch):
+    orig = ocg._U.__wrapped__
+
+    def badU(l):
+        U = orig(l).copy()
+        if l >= 1:
+            U[0, :] = -1j * U[0, :]  # plant: wrong phase on the m=-l row
+        return U
+    monkeypatch.setattr(ocg, "_U", badU)
+    try:
+        ok = _cross_relation_holds() and _equivariant()
+    except AssertionError:
+        ok = False  # the real/imaginary dichotomy check inside the oracle fired
+    assert not ok
+
+
+def test_swapped_operands_are_caught(monkeypatch):
+    orig = ocg._real_block.__wrapped__
+    monkeypatch.setattr(ocg, "_real_block",
+                        lambda l1, l2, J: orig(l2, l1, J).transpose(0, 2, 1) if l1 == l2 else orig(l1, l2, J))
+    # k (x) q instead of q (x) k flips every odd path: the §4.4 sign fails
+    assert not _cross_relation_holds()
+
+
+def test_dropped_odd_paths_are_caught(monkeypatch):
+    orig = ocg._real_block.__wrapped__
+    monkeypatch.setattr(ocg, "_real_block",
+                        lambda l1, l2, J: orig(l1, l2, J) * ((l1 + l2 + J) % 2 == 0))
+    assert not _cross_relation_holds()
+
+
+def test_correlation_instead_of_convolution_is_caught(monkeypatch):
+    rng = np.random.default_rng(2)
+    q, k = rng.normal(size=(1, 8, 4, 2)), rng.normal(size=(1, 8, 4, 2))
+    ref_fft = oconv.cgconv_fft(q, k, 1)
+
+    def bad_rows(qb, kb, i_list, RK):
+        N, K, C = qb.shape
+        j = np.arange(N)
+        out = np.empty((len(i_list), K, C))
+        for n, i in enumerate(i_list):
+            ks = kb[(i + j) % N]  # plant: i + j
+            P = np.matmul(np.transpose(qb, (2, 1, 0)), np.transpose(ks, (2, 0, 1)))
+            out[n] = (P.reshape(C, K * K) @ RK.T).T
+        return out
+    monkeypatch.setattr(oconv, "_rows_direct", bad_rows)
+    bad = oconv.cgconv_direct(q, k, 1)
+    assert np.abs(bad - ref_fft).max() > 1e-6
+
+
+def test_wrong_racah_prefactor_is_caught(monkeypatch):
+    def bad(l1, m1, l2, m2, J, M):
+        if M != m1 + m2 or not (abs(l1 - l2) <= J <= l1 + l2) or abs(M) > J:
+            return 0.0
+        f = factorial
+        pre = (2 * J + 1) * f(J + l1 - l2) * f(J - l1 + l2) * f(l1 + l2 - J) / f(l1 + l2 + J)  # plant: +1 dropped
+        pre *= f(J + M) * f(J - M) * f(l1 - m1) * f(l1 + m1) * f(l2 - m2) * f(l2 + m2)
+        s = 0.0
+        for t in range(0, l1 + l2 + J + 1):
+            args = (t, l1 + l2 - J - t, l1 - m1 - t, l2 + m2 - t, J - l2 + m1 + t, J - l1 - m2 + t)
+            if min(args) < 0:
+                continue
+            d = 1
+            for a in args:
+                d *= f(a)
+            s += (-1) ** t / d
+        return np.sign(s) * sqrt(pre * s * s)
+    monkeypatch.setattr(ocg, "cg_complex", bad)
+    assert not _orthogonal()
