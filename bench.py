@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Throughput benchmark of the global CG convolution on one MI355X.
+
+Workload (the configuration the headline metric is quoted on): point-cloud
+token sets, B=8, N=16384 tokens, L_max=6 (49 components), C=32 channels,
+fp32 -- synthetic inputs shaped like the paper's point-cloud experiments
+(features = real spherical harmonics of ellipsoid surface normals times
+per-channel weights; see workloads/).  One step = one cgconv_forward of the
+whole batch (forward DFTs, sparse CG product, inverse DFTs), inputs already
+resident in HBM.
+
+Prints ONE JSON line.  Besides the contract fields it carries
+  roofline      the dominant kernel (the CG stage, VALU-bound) against the
+                fp32 FMA issue rate, timed live with HIP events on the stream
+                the kernels run on; traffic from the committed rocprofv3
+                counter summary if it was taken on the current kernel source
+  stages        per-stage average time and achieved bandwidth of each kernel
+  cpu_baseline  the CPU oracle (direct O(N^2) definition) on sampled output
+                rows of the same inputs; those rows also check the GPU output
+Flags: --gpus N (only 1 is supported), --steps K, --warmup W,
+--no-cpu-baseline, --cpu-seconds S, --workload NAME (other synthetic
+workloads, for exploration), --bf16, --copy-calibration (a plain device copy
+of known size, the reference for rocprofv3 byte counters).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+# fp32 FMA issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz.  The
+# published 157.3 TFLOP/s "vector fp32" counts packed-fp32 dual issue, which
+# this build does not use (packed fp32 instructions are disabled).
+VALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+VALU_PEAK_PACKED_TFLOPS = 157.3
+METRIC = "CG-conv tokens/sec at N=16384, L_max=6, C=32; achieved HBM GB/s vs peak"
+CG_SOURCES = ["paper_2509_24093_amd/csrc/cg_gen.hip", "paper_2509_24093_amd/csrc/cg_common.h",
+              "paper_2509_24093_amd/csrc/codegen/gen_cg.cpp", "paper_2509_24093_amd/csrc/cg_table.cpp",
+              "paper_2509_24093_amd/csrc/kernels.h"]
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "cg_kernel_pointcloud_pmc.md")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cg_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in CG_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload):
+    """HBM bytes per CG launch from the committed rocprofv3 counter summary,
+    if it was taken on the current CG kernel source and this workload."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None, "no counter summary committed"
+    text = open(PMC_SUMMARY).read()
+    start = text.find("```json")
+    if start < 0:
+        return None, "counter summary has no json block"
+    end = text.find("```", start + 7)
+    d = json.loads(text[start + 7:end])
+    if d.get("cg_source_hash") != cg_source_hash():
+        return None, "CG kernel changed since the counters were taken"
+    if d.get("workload") != workload:
+        return None, "counters were taken on another workload"
+    return d["cg_hbm_bytes_per_launch"], "rocprofv3 FETCH_SIZE+WRITE_SIZE, copy-calibrated"
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 28  # 1 GiB of fp32
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}), flush=True)
+
+
+def cpu_baseline(q, k, L, budget_s, got):
+    """Oracle direct mode on sampled output rows; returns the bench object and
+    the parity of the GPU output on those rows."""
+    import numpy as np
+    from oracle.conv import cgconv_direct_rows
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
+    except Exception:
+        blas_threads = None
+    B, N = q.shape[0], q.shape[1]
+    rng = np.random.default_rng(2024)
+    rows = [(0, 0), (B - 1, N - 1)] + [(int(rng.integers(B)), int(rng.integers(N))) for _ in range(254)]
+    t0 = time.perf_counter()
+    cgconv_direct_rows(q, k, L, rows[:1])
+    t1 = time.perf_counter()
+    per_row = t1 - t0
+    R = int(max(2, min(len(rows), budget_s / max(per_row, 1e-6))))
+    t0 = time.perf_counter()
+    ref = cgconv_direct_rows(q, k, L, rows[:R])
+    dt = time.perf_counter() - t0
+    num = den = 0.0
+    for n, (b, i) in enumerate(rows[:R]):
+        d = got[b, i].astype(np.float64) - ref[n]
+        num += float((d * d).sum())
+        den += float((ref[n] * ref[n]).sum())
+    cores = len(os.sched_getaffinity(0))
+    obj = {"value": R / dt, "unit": "tokens/s", "cores": blas_threads or cores, "kind": "oracle",
+           "sample": f"direct O(N^2) definition on {R} sampled output rows (b, i) of the same workload "
+                     f"(all K components and C channels per row), fp64 numpy, {dt:.1f} s; "
+                     f"host exposes {cores} cores"}
+    return obj, (num / den) ** 0.5 if den > 0 else 0.0, R
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="pointcloud")
+    ap.add_argument("--bf16", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} is not supported: this build runs on one GPU only "
+              "(the path shards over batch and channels with no exchange; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2509_24093_amd as P
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    w = W.WORKLOADS[args.workload]
+    B, N, L, C = w["B"], w["N"], w["L"], w["C"]
+    K = (L + 1) ** 2
+    log(f"[bench] generating {args.workload} inputs B={B} N={N} L={L} C={C}")
+    q, k = W.make(args.workload)
+    if args.bf16:
+        qd = torch.from_numpy(W.to_bf16_bits(q).view(np.int16)).cuda().view(torch.bfloat16)
+        kd = torch.from_numpy(W.to_bf16_bits(k).view(np.int16)).cuda().view(torch.bfloat16)
+        esize = 2
+    else:
+        qd = torch.from_numpy(q).cuda()
+        kd = torch.from_numpy(k).cuda()
+        esize = 4
+    out = torch.empty_like(qd)
+    plan = P.Plan(B, N, L, C)
+    n_paths, nnz, n_products, ws_bytes = plan.info()
+    log(f"[bench] plan: paths={n_paths} nnz={nnz} products={n_products} workspace={ws_bytes / 2**30:.2f} GiB")
+
+    for _ in range(args.warmup):
+        plan(qd, kd, out)
+    torch.cuda.synchronize()
+    plan.enable_timing(args.steps)
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        plan(qd, kd, out)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    stage_ms, ncalls = plan.stage_times()
+    stage_avg = {s: v / max(ncalls, 1) for s, v in stage_ms.items()}
+    tokens = B * N
+    S = B * N * K * C * esize                     # one feature tensor in bytes
+    # bytes each kernel must move (inputs read + outputs written), fp32 spectra
+    Sc = B * N * K * C * 4
+    Cp = (C + 1) // 2
+    Sp = B * N * K * Cp * 8
+    io = ({"fft_fwd_1": 2 * S + 2 * Sc, "fft_fwd_2": 4 * Sc, "cg": 2 * Sc + Sp, "fft_inv_1": 2 * Sp,
+           "fft_inv_2": Sp + S} if N > 256 else
+          {"fft_fwd": 2 * S + 2 * Sc, "cg": 2 * Sc + Sp, "fft_inv": Sp + S})
+    stages = {s: {"ms": round(t, 4), "bytes": io.get(s), "gbs": round(io.get(s, 0) / (t * 1e-3) / 1e9, 1)}
+              for s, t in stage_avg.items()}
+    F = N // 2 + 1
+    points = B * F * C
+    cg_flops_per_point = 6 * n_products + 4 * nnz
+    cg_ms = stage_avg["cg"]
+    achieved_tflops = points * cg_flops_per_point / (cg_ms * 1e-3) / 1e12
+    traffic, traffic_src = committed_traffic(args.workload) if not args.bf16 else (None, "bf16 run")
+    roofline = {
+        "kernel": f"cg_gen_kernel<{L}>",
+        "bound": "alu",
+        "achieved": round(achieved_tflops, 2),
+        "peak": round(VALU_PEAK_TFLOPS, 1),
+        "unit": "TFLOP/s",
+        "frac": round(achieved_tflops / VALU_PEAK_TFLOPS, 4),
+        "traffic": traffic,
+        "traffic_source": traffic_src,
+        "flops_per_launch": points * cg_flops_per_point,
+        "flop_model": f"(6*{n_products} distinct complex products + 4*{nnz} non-zeros) per "
+                      f"(b, frequency 0..N/2, channel) point, {points} points",
+        "launch_ms": round(cg_ms, 4),
+        "frac_of_packed_fp32_peak": round(achieved_tflops / VALU_PEAK_PACKED_TFLOPS, 4),
+    }
+    hbm_alg_gbs = 3 * S / (ms * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": tokens / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16-storage/f32" if args.bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C,
+                   "parallelism": "single GPU"},
+        "hbm": {"algorithmic_bytes_per_step": 3 * S, "achieved_gbs": round(hbm_alg_gbs, 1),
+                "peak_gbs": HBM_PEAK_GBS, "frac": round(hbm_alg_gbs / HBM_PEAK_GBS, 4)},
+        "roofline": roofline,
+        "stages": stages,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] CPU oracle baseline (~{args.cpu_seconds:.0f} s)")
+        got = out.float().cpu().numpy() if args.bf16 else out.cpu().numpy()
+        if args.bf16:
+            q = W.bf16_bits_to_f32(W.to_bf16_bits(q))
+            k = W.bf16_bits_to_f32(W.to_bf16_bits(k))
+        obj, parity, R = cpu_baseline(q, k, L, args.cpu_seconds, got)
+        result["cpu_baseline"] = obj
+        result["parity_rel_l2_sampled_rows"] = parity
+        log(f"[bench] parity on {R} rows: rel_l2 = {parity:.3e}")
+    else:
+        result["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

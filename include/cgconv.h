@@ -1,0 +1,142 @@
+/*
+ * cgconv.h - C ABI of the MI355X (gfx950) global Clebsch-Gordan convolution.
+ *
+ * The operation (arXiv 2509.24093, §4.1, Eq. (EquiConv) summed over every
+ * path as in the path sum that follows it; FFT / tensor product / inverse FFT
+ * as in Algorithm 1):
+ *
+ *   out[b,i,(J,M),c] = sum_{l1,l2} sum_{m1,m2} R^{(l1 l2 J)}[M,m1,m2]
+ *                      * sum_j q[b,j,(l1,m1),c] * k[b,(i-j) mod N,(l2,m2),c]
+ *
+ * for every output degree J = 0..L_max and every triangle-allowed path
+ * (|l1-l2| <= J <= l1+l2, l1,l2 <= L_max, odd l1+l2+J included), with unit
+ * path weights, a cyclic token boundary and depthwise channels (channel c of q
+ * meets only channel c of k; §4.1 "intra-channel").  R is the real-basis
+ * Clebsch-Gordan tensor: real harmonics with Y_1 ~ (y, z, x), sign fixed so
+ * that the (1,1 -> 1) path is +(1/sqrt 2) q x k (§4.4).  Sparsity follows
+ * §4.3: only coefficients obeying the selection rule M = m1 + m2 (complex
+ * basis) are evaluated.
+ *
+ * Layout of q, k, out: contiguous [batch][N][(L_max+1)^2][C], component index
+ * l*l + l + m, channel fastest.  All pointers are DEVICE pointers, 16-byte
+ * aligned.  Ownership: the caller owns q, k, out and the stream; a plan owns
+ * its device workspace and tables.
+ *
+ * Errors: functions returning int give 0 on success or a negative
+ * cgconv_status; cgconv_last_error() returns a thread-local message for the
+ * last failure on the calling thread.  No C++ exception crosses this ABI.
+ * Kernel faults are asynchronous and surface at the caller's next
+ * synchronisation of the stream.
+ */
+#ifndef CGCONV_H
+#define CGCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hipStream_t; /* same opaque type as HIP's */
+typedef struct cgconv_plan* cgconv_plan_t;
+
+enum cgconv_status {
+  CGCONV_OK = 0,
+  CGCONV_ERR_INVALID_ARG = -1,   /* null handle/pointer, bad size */
+  CGCONV_ERR_UNSUPPORTED = -2,   /* N not a power of two, N too large, L_max too large */
+  CGCONV_ERR_ALIGNMENT = -3,     /* a pointer is not 16-byte aligned */
+  CGCONV_ERR_OUT_OF_MEMORY = -4, /* workspace allocation failed */
+  CGCONV_ERR_HIP = -5            /* a HIP runtime call failed */
+};
+
+/* Largest supported degree and token count. */
+#define CGCONV_LMAX 8
+#define CGCONV_NMAX 65536
+
+/*
+ * Create a plan for q, k, out of shape [batch][N][(L_max+1)^2][C].
+ * batch >= 1; N >= 2 and a power of two, N <= CGCONV_NMAX; 0 <= L_max <=
+ * CGCONV_LMAX; C >= 1.  Builds the sparse CG table (§4.3) and the FFT
+ * twiddles on the host, allocates the device workspace (hipMalloc on the
+ * current device, 2 * batch*N*(L_max+1)^2*C*8 bytes) and uploads the tables.
+ * Synchronous.  Returns NULL on failure (see cgconv_last_error()).
+ */
+cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_t C);
+
+/*
+ * Enqueue one CG convolution on `stream` (NULL = the legacy default stream),
+ * fp32 in, fp32 out, fp32 arithmetic.  Asynchronous: no host synchronisation.
+ * out must not alias q or k; q == k is allowed.  The plan's workspace is
+ * shared by its calls: do not have two forwards of one plan in flight on
+ * different streams.  The device current at plan creation must be current.
+ */
+int cgconv_forward(cgconv_plan_t plan, const float* q, const float* k, float* out,
+                   hipStream_t stream);
+
+/*
+ * As cgconv_forward, with q, k, out stored as bfloat16 bit patterns (uint16)
+ * and all arithmetic in fp32; the output is rounded to bfloat16 to nearest,
+ * ties to even.
+ */
+int cgconv_forward_bf16(cgconv_plan_t plan, const uint16_t* q, const uint16_t* k,
+                        uint16_t* out, hipStream_t stream);
+
+/* Free the plan's device workspace and tables.  NULL is a no-op. */
+void cgconv_plan_destroy(cgconv_plan_t plan);
+
+/*
+ * Plan introspection: number of CG paths (l1,l2,J); number of non-zero
+ * complex-basis coefficients the kernels evaluate per frequency and channel
+ * (selection rule M = m1 + m2, §4.3); number of distinct complex products
+ * q[l1,m1] * k[l2,m2] among them; workspace bytes.  Any output pointer may be
+ * NULL.
+ */
+int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths, int64_t* nnz, int64_t* n_products,
+                     size_t* workspace_bytes);
+
+/*
+ * Host-only (no GPU needed): the real-basis CG tensor R for degrees 0..L_max
+ * as the library builds it (§4.3 and the appendix on sparsity, real basis).
+ * Writes up to `cap` entries: idx[6*e .. 6*e+5] = (l1, m1, l2, m2, J, M) and
+ * coef[e], for every path and every |coefficient| > 1e-12, sorted by
+ * (J, M, l1, m1, l2, m2).  Returns the total number of entries (which may
+ * exceed cap; nothing beyond cap is written), or a negative status.
+ * idx/coef may be NULL when cap == 0.
+ */
+int64_t cgconv_cg_table(int32_t L_max, int32_t* idx, double* coef, int64_t cap);
+
+/*
+ * Host-only (no GPU needed) self-check of the frequency-domain contraction
+ * the kernels evaluate: given the spectra of q and k at one frequency for one
+ * channel (K complex values each, interleaved re,im, real-basis component
+ * order), writes the K complex output values.  It applies the same
+ * coefficient table, in double precision, that the generated GPU code
+ * carries.  cgconv_forward never calls it.
+ */
+int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, double* uhat);
+
+/*
+ * Per-stage timing for profiling.  After cgconv_plan_enable_timing(plan, n),
+ * the next n forwards of the plan record HIP events before and after each
+ * kernel stage on the forward's own stream (a few microseconds per call);
+ * calls beyond n are not timed.  Enabling again resets the record.
+ * cgconv_plan_stage_times waits for the timed calls to finish and writes the
+ * summed time of each stage in milliseconds to ms[0 .. min(cap, n_stages)-1];
+ * n_stages and n_calls (may be NULL) receive the stage count (3 for N <= 256:
+ * fft_fwd, cg, fft_inv; 5 above: fft_fwd_1, fft_fwd_2, cg, fft_inv_1,
+ * fft_inv_2) and the number of timed calls.  cgconv_plan_stage_name returns
+ * a stage's name ("" if out of range).
+ */
+int cgconv_plan_enable_timing(cgconv_plan_t plan, int32_t max_calls);
+int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t* n_stages, int32_t* n_calls);
+const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage);
+
+/* Thread-local message describing the last error on this thread ("" if none). */
+const char* cgconv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CGCONV_H */

@@ -1,0 +1,213 @@
+"""MI355X (gfx950) global Clebsch-Gordan convolution (arXiv 2509.24093, §4.1).
+
+Thin ctypes binding of ``libcgconv.so`` (built in-tree by ``build.py``).
+Every step of the computation runs in the library's HIP kernels; this module
+only marshals arguments.  PyTorch supplies device memory and the stream.
+There is no CPU fallback: if the library is missing, every entry point
+raises.
+
+The module-level functions carry the C ABI's names and arguments
+(``include/cgconv.h``); :class:`Plan` wraps them for torch tensors.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcgconv.so")
+
+CGCONV_OK = 0
+CGCONV_ERR_INVALID_ARG = -1
+CGCONV_ERR_UNSUPPORTED = -2
+CGCONV_ERR_ALIGNMENT = -3
+CGCONV_ERR_OUT_OF_MEMORY = -4
+CGCONV_ERR_HIP = -5
+CGCONV_LMAX = 8
+CGCONV_NMAX = 65536
+
+_lib = None
+
+
+class CgconvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"cgconv error {status}: {message}")
+        self.status = status
+
+
+def library() -> ctypes.CDLL:
+    """Load ``libcgconv.so`` (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2509_24093_amd.build` "
+                           "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    lib.cgconv_plan_create.argtypes = [i64, i64, i32, i64]
+    lib.cgconv_plan_create.restype = vp
+    lib.cgconv_forward.argtypes = [vp, vp, vp, vp, vp]
+    lib.cgconv_forward.restype = ctypes.c_int
+    lib.cgconv_forward_bf16.argtypes = [vp, vp, vp, vp, vp]
+    lib.cgconv_forward_bf16.restype = ctypes.c_int
+    lib.cgconv_plan_destroy.argtypes = [vp]
+    lib.cgconv_plan_destroy.restype = None
+    lib.cgconv_plan_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                     ctypes.POINTER(sz)]
+    lib.cgconv_plan_info.restype = ctypes.c_int
+    lib.cgconv_cg_table.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double), i64]
+    lib.cgconv_cg_table.restype = i64
+    lib.cgconv_contract_host.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_double)]
+    lib.cgconv_contract_host.restype = ctypes.c_int
+    lib.cgconv_plan_enable_timing.argtypes = [vp, i32]
+    lib.cgconv_plan_enable_timing.restype = ctypes.c_int
+    lib.cgconv_plan_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double), i32, ctypes.POINTER(i32),
+                                            ctypes.POINTER(i32)]
+    lib.cgconv_plan_stage_times.restype = ctypes.c_int
+    lib.cgconv_plan_stage_name.argtypes = [vp, i32]
+    lib.cgconv_plan_stage_name.restype = ctypes.c_char_p
+    lib.cgconv_last_error.argtypes = []
+    lib.cgconv_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+# ---- C ABI, same names -------------------------------------------------------
+
+def cgconv_last_error() -> str:
+    return library().cgconv_last_error().decode()
+
+
+def _check(status: int) -> int:
+    if status < 0:
+        raise CgconvError(status, cgconv_last_error())
+    return status
+
+
+def cgconv_plan_create(batch: int, N: int, L_max: int, C: int) -> int:
+    h = library().cgconv_plan_create(batch, N, L_max, C)
+    if not h:
+        raise CgconvError(CGCONV_ERR_INVALID_ARG, cgconv_last_error())
+    return h
+
+
+def cgconv_forward(plan: int, q: int, k: int, out: int, stream: int) -> int:
+    """Device pointers as integers; returns the status (raises on error)."""
+    return _check(library().cgconv_forward(plan, q, k, out, stream))
+
+
+def cgconv_forward_bf16(plan: int, q: int, k: int, out: int, stream: int) -> int:
+    return _check(library().cgconv_forward_bf16(plan, q, k, out, stream))
+
+
+def cgconv_plan_destroy(plan: int) -> None:
+    library().cgconv_plan_destroy(plan)
+
+
+def cgconv_plan_info(plan: int):
+    """Returns (n_paths, nnz, n_products, workspace_bytes)."""
+    a, b, c, d = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_size_t()
+    _check(library().cgconv_plan_info(plan, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c), ctypes.byref(d)))
+    return a.value, b.value, c.value, d.value
+
+
+def cgconv_plan_enable_timing(plan: int, max_calls: int) -> None:
+    _check(library().cgconv_plan_enable_timing(plan, max_calls))
+
+
+def cgconv_plan_stage_times(plan: int):
+    """Returns ({stage name: summed ms}, number of timed calls)."""
+    lib = library()
+    ms = (ctypes.c_double * 8)()
+    ns, nc = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib.cgconv_plan_stage_times(plan, ms, 8, ctypes.byref(ns), ctypes.byref(nc)))
+    return {lib.cgconv_plan_stage_name(plan, i).decode(): ms[i] for i in range(ns.value)}, nc.value
+
+
+def cgconv_cg_table(L_max: int):
+    """Real-basis CG non-zeros as built by the library (host only).
+    Returns (idx int32 (n, 6) = l1, m1, l2, m2, J, M; coef float64 (n,))."""
+    import numpy as np
+    lib = library()
+    n = _check(lib.cgconv_cg_table(L_max, None, None, 0))
+    idx = np.zeros((n, 6), dtype=np.int32)
+    coef = np.zeros(n, dtype=np.float64)
+    got = _check(lib.cgconv_cg_table(L_max, idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                     coef.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), n))
+    assert got == n
+    return idx, coef
+
+
+def cgconv_contract_host(L_max: int, qhat, khat):
+    """Host self-check of the frequency-domain contraction: qhat, khat complex
+    (K,) arrays; returns the complex (K,) output."""
+    import numpy as np
+    K = (L_max + 1) ** 2
+    q = np.ascontiguousarray(qhat, dtype=np.complex128)
+    k = np.ascontiguousarray(khat, dtype=np.complex128)
+    if q.shape != (K,) or k.shape != (K,):
+        raise ValueError(f"expected ({K},) complex arrays")
+    u = np.zeros(K, dtype=np.complex128)
+    P = ctypes.POINTER(ctypes.c_double)
+    _check(library().cgconv_contract_host(L_max, q.ctypes.data_as(P), k.ctypes.data_as(P), u.ctypes.data_as(P)))
+    return u
+
+
+# ---- torch convenience -------------------------------------------------------
+
+class Plan:
+    """A plan for q, k, out of shape [batch, N, (L_max+1)^2, C] on the current
+    GPU.  ``plan(q, k)`` returns out; fp32 or bfloat16 tensors."""
+
+    def __init__(self, batch: int, N: int, L_max: int, C: int):
+        self.shape = (int(batch), int(N), (int(L_max) + 1) ** 2, int(C))
+        self.L_max = int(L_max)
+        self._h = cgconv_plan_create(int(batch), int(N), int(L_max), int(C))
+
+    def info(self):
+        return cgconv_plan_info(self._h)
+
+    def enable_timing(self, max_calls: int):
+        cgconv_plan_enable_timing(self._h, max_calls)
+
+    def stage_times(self):
+        return cgconv_plan_stage_times(self._h)
+
+    def _args(self, q, k, out, dtype):
+        import torch
+        for name, t in (("q", q), ("k", k), ("out", out)):
+            if not isinstance(t, torch.Tensor) or not t.is_cuda:
+                raise ValueError(f"{name} must be a GPU tensor")
+            if tuple(t.shape) != self.shape or t.dtype != dtype or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {self.shape}")
+        return torch.cuda.current_stream().cuda_stream
+
+    def forward(self, q, k, out=None):
+        import torch
+        if out is None:
+            out = torch.empty(self.shape, dtype=q.dtype, device=q.device)
+        if q.dtype == torch.float32:
+            s = self._args(q, k, out, torch.float32)
+            cgconv_forward(self._h, q.data_ptr(), k.data_ptr(), out.data_ptr(), s)
+        elif q.dtype == torch.bfloat16:
+            s = self._args(q, k, out, torch.bfloat16)
+            cgconv_forward_bf16(self._h, q.data_ptr(), k.data_ptr(), out.data_ptr(), s)
+        else:
+            raise ValueError("q, k must be float32 or bfloat16")
+        return out
+
+    __call__ = forward
+
+    def close(self):
+        if getattr(self, "_h", None):
+            cgconv_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,118 @@
+// Frequency-domain sparse CG tensor product for gfx950 (arXiv 2509.24093,
+// §4.1 convolution theorem + §4.3 sparsity).
+//
+// Input: Z = DFT of z = q + i k along the tokens, [B][N][K][C] float2.
+// For every frequency pair (w, N-w), 0 <= w <= N/2, and channel c, one lane
+//   * unpacks the spectra  Q = (Z_w + conj Z_{N-w}) / 2,
+//                          K = (Z_w - conj Z_{N-w}) / (2i)   (kept as 2Q, 2K),
+//   * moves to the complex-m basis (one idempotent component, see
+//     cg_table.h), evaluates the sparse contraction (selection rule
+//     M = m1 + m2) and moves back to the real basis,
+//   * exchanges its result with the neighbouring lane (channel c^1) by DPP
+//     and writes the packed inverse-FFT input  W = U_c + i U_{c+1}:  the even
+//     lane writes frequency w, the odd lane frequency N-w (Hermitian symmetry
+//     of U gives W_{N-w} = conj U_c + i conj U_{c+1}).
+// Lanes run over channels fastest, so every load and store of a wavefront is
+// a contiguous run over the channel axis.
+#include <hip/hip_runtime.h>
+
+#include "cg_common.h"
+#include "cg_lgen.h"
+
+namespace cgconv {
+namespace {
+
+using namespace cgdev;
+
+// Table-driven contraction for any L_max <= 8: spectra staged in LDS,
+// one point per lane, terms read from a table (sorted by output index).
+constexpr int kGenThreads = 64;
+constexpr int kGenKmax = 81;
+
+__global__ __launch_bounds__(kGenThreads) void cg_generic_kernel(CgArgs a) {
+  __shared__ float2 sq[kGenKmax * kGenThreads];
+  __shared__ float2 sk[kGenKmax * kGenThreads];
+  const int K = a.K;
+  const int lane = threadIdx.x;
+  const long long p = (long long)blockIdx.x * kGenThreads + lane;
+  const Point pt = point_of(p, a);
+  {
+    const bool cv = pt.valid && pt.c < a.C;
+    const long long wn = (a.N - pt.w) & (a.N - 1);
+    const float2* za = a.Z + ((pt.b * a.N + pt.w) * K) * a.C + pt.c;
+    const float2* zb = a.Z + ((pt.b * a.N + wn) * K) * a.C + pt.c;
+    for (int k = 0; k < K; ++k) {
+      const float2 A = cv ? za[(long long)k * a.C] : make_float2(0.f, 0.f);
+      const float2 B = cv ? zb[(long long)k * a.C] : make_float2(0.f, 0.f);
+      sq[k * kGenThreads + lane] = make_float2(A.x + B.x, A.y - B.y);
+      sk[k * kGenThreads + lane] = make_float2(A.y + B.y, B.x - A.x);
+    }
+    for (int l = 1; l * l < K; ++l) {
+      for (int mu = 1; mu <= l; ++mu) {
+        const int c = (l * l + l + mu) * kGenThreads + lane, s = (l * l + l - mu) * kGenThreads + lane;
+        float2 xc = sq[c], xs = sq[s];
+        sq[s] = make_float2(xc.x - xs.y, xc.y + xs.x);
+        sq[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
+        xc = sk[c];
+        xs = sk[s];
+        sk[s] = make_float2(xc.x - xs.y, xc.y + xs.x);
+        sk[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
+      }
+    }
+  }
+  const PairStore st = make_store(a, pt, K);
+  auto accumulate = [&](int o) {
+    float2 acc = make_float2(0.f, 0.f);
+    for (int t = a.offs[o]; t < a.offs[o + 1]; ++t) {
+      const uint32_t key = a.tkey[t];
+      const float cf = a.tcoef[t];
+      const float2 x = sq[(key & 0xff) * kGenThreads + lane];
+      const float2 y = sk[((key >> 8) & 0xff) * kGenThreads + lane];
+      const float pr = fmaf(-x.y, y.y, x.x * y.x), pi = fmaf(x.y, y.x, x.x * y.y);
+      if (key >> 16) {
+        acc.x = fmaf(-cf, pi, acc.x);
+        acc.y = fmaf(cf, pr, acc.y);
+      } else {
+        acc.x = fmaf(cf, pr, acc.x);
+        acc.y = fmaf(cf, pi, acc.y);
+      }
+    }
+    return acc;
+  };
+  for (int J = 0; J * J < K; ++J) {
+    st(J * J + J, accumulate(J * J + J));
+    for (int mu = 1; mu <= J; ++mu) {
+      const float2 wp = accumulate(J * J + J + mu), wm = accumulate(J * J + J - mu);
+      st(J * J + J + mu, make_float2(wm.x + wp.x, wm.y + wp.y));
+      st(J * J + J - mu, make_float2(wm.y - wp.y, wp.x - wm.x));
+    }
+  }
+}
+
+}  // namespace
+
+int cg_generated_lmax() { return CGCONV_LGEN; }
+
+hipError_t launch_cg(int L, const CgArgs& a, bool force_generic, hipStream_t s) {
+  if (a.npts <= 0) return hipSuccess;
+  if (!force_generic && L <= CGCONV_LGEN) {
+    switch (L) {
+      case 0: return launch_cg_gen<0>(a, s);
+      case 1: return launch_cg_gen<1>(a, s);
+      case 2: return launch_cg_gen<2>(a, s);
+      case 3: return launch_cg_gen<3>(a, s);
+      case 4: return launch_cg_gen<4>(a, s);
+      case 5: return launch_cg_gen<5>(a, s);
+      case 6: return launch_cg_gen<6>(a, s);
+      case 7: return launch_cg_gen<7>(a, s);
+      case 8: return launch_cg_gen<8>(a, s);
+      default: break;
+    }
+  }
+  if (a.K > kGenKmax || a.offs == nullptr) return hipErrorInvalidValue;
+  const long long blocks = (a.npts + kGenThreads - 1) / kGenThreads;
+  hipLaunchKernelGGL(cg_generic_kernel, dim3((unsigned)blocks), dim3(kGenThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace cgconv

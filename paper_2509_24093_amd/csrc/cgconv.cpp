@@ -1,0 +1,472 @@
+// Plan and C ABI of the global CG convolution (see include/cgconv.h).
+//
+// Forward pipeline for one call, all on the caller's stream:
+//   N <= 256 : DFT(z = q + i k) -> CG stage -> inverse DFT (x 1/N, split)
+//   N  > 256 : N = N1 * N2 four-step factorisation with n = n2 + N2 n1 and
+//              w = w1 + N1 w2:
+//     F1  for each n2: length-N1 DFT over n1, twiddle W_N^(n2 w1)   q,k -> Y
+//     F2  for each w1: length-N2 DFT over n2                         Y -> Z
+//     CG  sparse tensor product per frequency pair and channel       Z -> W
+//     I1  for each w1: inverse length-N2 DFT, twiddle W_N^(-n2 w1)   W -> V
+//     I2  for each n2: inverse length-N1 DFT, x 1/N, split channels  V -> out
+// Y, Z, W, V live in two plan-owned workspaces of B*N*K*C float2 each.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <complex>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/cgconv.h"
+#include "cg_table.h"
+#include "kernels.h"
+
+using namespace cgconv;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+}
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+int ilog2(int64_t x) {
+  int r = 0;
+  while ((int64_t(1) << r) < x) ++r;
+  return r;
+}
+
+}  // namespace
+
+struct cgconv_plan {
+  int64_t B = 0, N = 0, C = 0, Cp = 0;
+  int L = 0, K = 0;
+  int64_t N1 = 0, N2 = 0;  // N1 == 0: single pass
+  int device = 0;
+  int64_t nnz = 0, paths = 0, products = 0;
+  size_t ws_bytes = 0;
+  float2* tw = nullptr;
+  float2* ws1 = nullptr;
+  float2* ws2 = nullptr;
+  int* d_offs = nullptr;
+  uint32_t* d_tkey = nullptr;
+  float* d_tcoef = nullptr;
+  bool force_generic = false;
+  // optional per-stage timing: events recorded on the forward's stream
+  int n_stages = 0;
+  int timing_max = 0, timing_calls = 0;
+  std::vector<hipEvent_t> events;  // timing_max * (n_stages + 1)
+};
+
+namespace {
+
+void free_plan(cgconv_plan* p) {
+  if (!p) return;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  (void)hipSetDevice(p->device);
+  (void)hipFree(p->tw);
+  (void)hipFree(p->ws1);
+  (void)hipFree(p->ws2);
+  (void)hipFree(p->d_offs);
+  (void)hipFree(p->d_tkey);
+  (void)hipFree(p->d_tcoef);
+  for (hipEvent_t ev : p->events) (void)hipEventDestroy(ev);
+  (void)hipSetDevice(cur);
+  delete p;
+}
+
+const char* const kStages2[] = {"fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"};
+const char* const kStages1[] = {"fft_fwd", "cg", "fft_inv"};
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+template <class T>
+hipError_t upload(T** dst, const std::vector<T>& src) {
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(dst), src.size() * sizeof(T));
+  if (e != hipSuccess) return e;
+  return hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+}
+
+PassArgs base_args(const cgconv_plan* p) {
+  PassArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.tw = p->tw;
+  a.C = (int)p->C;
+  a.Cp = (int)p->Cp;
+  a.KC = (int)(p->K * p->C);
+  a.Nmask = (int)(p->N - 1);
+  a.scale = 1.0f;
+  return a;
+}
+
+int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf16, hipStream_t s) {
+  const int K = p->K;
+  const long long Wz = (long long)K * p->C;   // complex columns of z
+  const long long Ww = (long long)K * p->Cp;  // complex columns of the packed output spectra
+  const int in_pair = bf16 ? IN_PAIR_BF16 : IN_PAIR_F32;
+  const int out_split = bf16 ? OUT_SPLIT_BF16 : OUT_SPLIT_F32;
+  hipError_t e;
+  auto pass = [&](int R, int inm, int outm, int dir, int groups, const void* in0, const void* in1, void* o,
+                  long long ib, long long ob, int W, int gs_in, int es_in, int gs_out, int fs_out, int inter,
+                  float scale) {
+    PassDesc d;
+    d.R = R;
+    d.in_mode = inm;
+    d.out_mode = outm;
+    d.dir = dir;
+    d.groups = groups;
+    d.batch = (int)p->B;
+    d.a = base_args(p);
+    d.a.in0 = in0;
+    d.a.in1 = in1;
+    d.a.out = o;
+    d.a.in_bstride = ib;
+    d.a.out_bstride = ob;
+    d.a.W = W;
+    d.a.gs_in = gs_in;
+    d.a.es_in = es_in;
+    d.a.gs_out = gs_out;
+    d.a.fs_out = fs_out;
+    d.a.tw_stride = (int)(p->N / R);
+    d.a.inter = inter;
+    d.a.scale = scale;
+    return launch_fft_pass(d, s);
+  };
+  CgArgs ca;
+  ca.N = p->N;
+  ca.F = p->N / 2 + 1;
+  ca.K = K;
+  ca.C = (int)p->C;
+  ca.Cp = (int)p->Cp;
+  ca.npts = p->B * ca.F * 2 * p->Cp;
+  ca.offs = p->d_offs;
+  ca.tkey = p->d_tkey;
+  ca.tcoef = p->d_tcoef;
+  const long long N = p->N;
+  const float inv_n = 1.0f / (float)N;
+  hipEvent_t* ev = nullptr;  // events of this call if it is timed
+  if (p->timing_calls < p->timing_max) {
+    ev = &p->events[(size_t)p->timing_calls * (p->n_stages + 1)];
+    ++p->timing_calls;
+  }
+  int stage = 0;
+  auto mark = [&]() {
+    if (ev) (void)hipEventRecord(ev[stage], s);
+    ++stage;
+  };
+  mark();
+  if (p->N1 == 0) {
+    e = pass((int)N, in_pair, OUT_COMPLEX, -1, 1, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 0, 1, 0, 1, 0, 1.0f);
+    if (e != hipSuccess) goto fail;
+    mark();
+    ca.Z = p->ws1;
+    ca.W = p->ws2;
+    ca.trash = p->ws2 + p->B * N * K * p->Cp;
+    e = launch_cg(p->L, ca, p->force_generic, s);
+    if (e != hipSuccess) goto fail;
+    mark();
+    e = pass((int)N, IN_COMPLEX, out_split, 1, 1, p->ws2, nullptr, out, N * Ww, N * K * p->C, (int)Ww, 0, 1, 0, 1,
+             0, inv_n);
+    if (e != hipSuccess) goto fail;
+    mark();
+  } else {
+    const int N1 = (int)p->N1, N2 = (int)p->N2;
+    e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
+    if (e != hipSuccess) goto fail;
+    mark();
+    e = pass(N2, IN_COMPLEX, OUT_COMPLEX, -1, N1, p->ws1, nullptr, p->ws2, N * Wz, N * Wz, (int)Wz, N2, 1, 1, N1, 0,
+             1.0f);
+    if (e != hipSuccess) goto fail;
+    mark();
+    ca.Z = p->ws2;
+    ca.W = p->ws1;
+    ca.trash = p->ws1 + p->B * N * K * p->Cp;
+    e = launch_cg(p->L, ca, p->force_generic, s);
+    if (e != hipSuccess) goto fail;
+    mark();
+    e = pass(N2, IN_COMPLEX, OUT_COMPLEX, 1, N1, p->ws1, nullptr, p->ws2, N * Ww, N * Ww, (int)Ww, 1, N1, N2, 1, 1,
+             1.0f);
+    if (e != hipSuccess) goto fail;
+    mark();
+    e = pass(N1, IN_COMPLEX, out_split, 1, N2, p->ws2, nullptr, out, N * Ww, N * K * p->C, (int)Ww, 1, N2, 1, N2, 0,
+             inv_n);
+    if (e != hipSuccess) goto fail;
+    mark();
+  }
+  return CGCONV_OK;
+fail:
+  set_error("kernel launch failed: %s", hipGetErrorString(e));
+  return CGCONV_ERR_HIP;
+}
+
+int check_forward_args(cgconv_plan* p, const void* q, const void* k, const void* out) {
+  if (!p) {
+    set_error("plan is NULL");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!q || !k || !out) {
+    set_error("q, k and out must be non-NULL device pointers");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!aligned16(q) || !aligned16(k) || !aligned16(out)) {
+    set_error("q, k and out must be 16-byte aligned");
+    return CGCONV_ERR_ALIGNMENT;
+  }
+  if (out == q || out == k) {
+    set_error("out must not alias q or k");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != p->device) {
+    set_error("the plan's device (%d) is not current (%d)", p->device, cur);
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  return CGCONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cgconv_last_error(void) { return g_last_error.c_str(); }
+
+cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_t C) {
+  g_last_error.clear();
+  if (batch < 1 || C < 1 || N < 2) {
+    set_error("invalid sizes: batch=%lld N=%lld C=%lld (need batch>=1, N>=2, C>=1)", (long long)batch,
+              (long long)N, (long long)C);
+    return nullptr;
+  }
+  if (L_max < 0) {
+    set_error("invalid L_max=%d", L_max);
+    return nullptr;
+  }
+  if (!is_pow2(N) || N > CGCONV_NMAX) {
+    set_error("unsupported N=%lld: need a power of two <= %d", (long long)N, CGCONV_NMAX);
+    return nullptr;
+  }
+  if (L_max > CGCONV_LMAX) {
+    set_error("unsupported L_max=%d: at most %d", L_max, CGCONV_LMAX);
+    return nullptr;
+  }
+  const int K = (L_max + 1) * (L_max + 1);
+  const int64_t Cp = (C + 1) / 2;
+  // sizes must keep every element index and grid dimension in range
+  const long double elems = (long double)batch * N * K * C;
+  if (elems > 4.0e9L || batch > 65535) {
+    set_error("problem too large: batch*N*K*C=%.3Le (max 4e9), batch=%lld (max 65535)", elems, (long long)batch);
+    return nullptr;
+  }
+  cgconv_plan* p = new (std::nothrow) cgconv_plan;
+  if (!p) {
+    set_error("host allocation failed");
+    return nullptr;
+  }
+  p->B = batch;
+  p->N = N;
+  p->C = C;
+  p->Cp = Cp;
+  p->L = L_max;
+  p->K = K;
+  if (N > 256) {
+    const int lg = ilog2(N);
+    p->N1 = int64_t(1) << ((lg + 1) / 2);
+    p->N2 = N / p->N1;
+  }
+  p->n_stages = p->N1 ? 5 : 3;
+  if (const char* env = std::getenv("CGCONV_FORCE_GENERIC")) p->force_generic = env[0] == '1';
+  hipError_t e = hipGetDevice(&p->device);
+  if (e != hipSuccess) {
+    set_error("hipGetDevice failed: %s", hipGetErrorString(e));
+    delete p;
+    return nullptr;
+  }
+  // twiddles exp(-2 pi i j / N), computed in double and rounded once
+  std::vector<float2> tw(N);
+  for (int64_t j = 0; j < N; ++j) {
+    const double ang = -2.0 * M_PI * (double)j / (double)N;
+    tw[j] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+  }
+  // table for the generic contraction kernel, grouped by complex-basis output
+  std::vector<Term> terms = contraction_terms(L_max);
+  std::vector<int> offs(K + 1, 0);
+  std::vector<uint32_t> tkey(terms.size());
+  std::vector<float> tcoef(terms.size());
+  for (const Term& t : terms) offs[comp(t.J, t.M) + 1]++;
+  for (int o = 0; o < K; ++o) offs[o + 1] += offs[o];
+  {
+    std::vector<int> fill(offs.begin(), offs.end() - 1);
+    for (const Term& t : terms) {
+      const int pos = fill[comp(t.J, t.M)]++;
+      tkey[pos] = (uint32_t)comp(t.l1, t.m1) | ((uint32_t)comp(t.l2, t.m2) << 8) | ((t.imag ? 1u : 0u) << 16);
+      tcoef[pos] = (float)t.coef;
+    }
+  }
+  p->nnz = (int64_t)terms.size();
+  {
+    std::vector<char> seen((size_t)K * K, 0);
+    for (const Term& t : terms) {
+      char& f = seen[(size_t)comp(t.l1, t.m1) * K + comp(t.l2, t.m2)];
+      p->products += f == 0;
+      f = 1;
+    }
+  }
+  p->paths = n_paths(L_max);
+  // each workspace holds a [B][N][K][C] float2 array, followed by a trash area
+  // of K*Cp float2 that absorbs the masked stores of the CG stage
+  const size_t ws = ((size_t)batch * N * K * C + (size_t)K * Cp) * sizeof(float2);
+  p->ws_bytes = 2 * ws;
+  if (const char* env = std::getenv("CGCONV_TEST_FAIL_ALLOC"); env && env[0] == '1') {
+    set_error("workspace allocation of %zu bytes failed (forced by CGCONV_TEST_FAIL_ALLOC)", p->ws_bytes);
+    delete p;
+    return nullptr;
+  }
+  if ((e = hipMalloc(&p->ws1, ws)) != hipSuccess || (e = hipMalloc(&p->ws2, ws)) != hipSuccess) {
+    set_error("workspace allocation of %zu bytes failed: %s", p->ws_bytes, hipGetErrorString(e));
+    (void)hipGetLastError();
+    free_plan(p);
+    return nullptr;
+  }
+  if ((e = upload(&p->tw, tw)) != hipSuccess || (e = upload(&p->d_offs, offs)) != hipSuccess ||
+      (e = upload(&p->d_tkey, tkey)) != hipSuccess || (e = upload(&p->d_tcoef, tcoef)) != hipSuccess) {
+    set_error("table upload failed: %s", hipGetErrorString(e));
+    free_plan(p);
+    return nullptr;
+  }
+  return p;
+}
+
+void cgconv_plan_destroy(cgconv_plan_t plan) { free_plan(plan); }
+
+int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths_out, int64_t* nnz, int64_t* n_products,
+                     size_t* workspace_bytes) {
+  if (!plan) {
+    set_error("plan is NULL");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (n_paths_out) *n_paths_out = plan->paths;
+  if (nnz) *nnz = plan->nnz;
+  if (n_products) *n_products = plan->products;
+  if (workspace_bytes) *workspace_bytes = plan->ws_bytes;
+  return CGCONV_OK;
+}
+
+int cgconv_plan_enable_timing(cgconv_plan_t plan, int32_t max_calls) {
+  if (!plan || max_calls < 0) {
+    set_error("plan is NULL or max_calls < 0");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  for (hipEvent_t ev : plan->events) (void)hipEventDestroy(ev);
+  plan->events.clear();
+  plan->timing_max = 0;
+  plan->timing_calls = 0;
+  const size_t n = (size_t)max_calls * (plan->n_stages + 1);
+  plan->events.reserve(n);
+  for (size_t i = 0; i < n; ++i) {
+    hipEvent_t ev;
+    const hipError_t e = hipEventCreate(&ev);
+    if (e != hipSuccess) {
+      set_error("hipEventCreate failed: %s", hipGetErrorString(e));
+      for (hipEvent_t x : plan->events) (void)hipEventDestroy(x);
+      plan->events.clear();
+      return CGCONV_ERR_HIP;
+    }
+    plan->events.push_back(ev);
+  }
+  plan->timing_max = max_calls;
+  return CGCONV_OK;
+}
+
+int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t* n_stages, int32_t* n_calls) {
+  if (!plan || (cap > 0 && !ms)) {
+    set_error("plan is NULL or ms is NULL");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const int ns = plan->n_stages;
+  if (n_stages) *n_stages = ns;
+  if (n_calls) *n_calls = plan->timing_calls;
+  for (int st = 0; st < cap && st < ns; ++st) ms[st] = 0.0;
+  for (int c = 0; c < plan->timing_calls; ++c) {
+    hipEvent_t* ev = &plan->events[(size_t)c * (ns + 1)];
+    hipError_t e = hipEventSynchronize(ev[ns]);
+    if (e != hipSuccess) {
+      set_error("hipEventSynchronize failed: %s", hipGetErrorString(e));
+      return CGCONV_ERR_HIP;
+    }
+    for (int st = 0; st < cap && st < ns; ++st) {
+      float t = 0.f;
+      e = hipEventElapsedTime(&t, ev[st], ev[st + 1]);
+      if (e != hipSuccess) {
+        set_error("hipEventElapsedTime failed: %s", hipGetErrorString(e));
+        return CGCONV_ERR_HIP;
+      }
+      ms[st] += t;
+    }
+  }
+  return CGCONV_OK;
+}
+
+const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
+  if (!plan || stage < 0 || stage >= plan->n_stages) return "";
+  return plan->N1 ? kStages2[stage] : kStages1[stage];
+}
+
+int cgconv_forward(cgconv_plan_t plan, const float* q, const float* k, float* out, hipStream_t stream) {
+  const int st = check_forward_args(plan, q, k, out);
+  if (st != CGCONV_OK) return st;
+  return run_forward(plan, q, k, out, false, stream);
+}
+
+int cgconv_forward_bf16(cgconv_plan_t plan, const uint16_t* q, const uint16_t* k, uint16_t* out,
+                        hipStream_t stream) {
+  const int st = check_forward_args(plan, q, k, out);
+  if (st != CGCONV_OK) return st;
+  return run_forward(plan, q, k, out, true, stream);
+}
+
+int64_t cgconv_cg_table(int32_t L_max, int32_t* idx, double* coef, int64_t cap) {
+  if (L_max < 0 || L_max > CGCONV_LMAX) {
+    set_error("unsupported L_max=%d", L_max);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  if (cap < 0 || (cap > 0 && (!idx || !coef))) {
+    set_error("invalid output buffers");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const std::vector<RealEntry> t = real_table(L_max);
+  for (int64_t e = 0; e < (int64_t)t.size() && e < cap; ++e) {
+    const RealEntry& r = t[e];
+    const int32_t v[6] = {r.l1, r.m1, r.l2, r.m2, r.J, r.M};
+    std::memcpy(idx + 6 * e, v, sizeof v);
+    coef[e] = r.coef;
+  }
+  return (int64_t)t.size();
+}
+
+int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, double* uhat) {
+  if (L_max < 0 || L_max > CGCONV_LMAX) {
+    set_error("unsupported L_max=%d", L_max);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  if (!qhat || !khat || !uhat) {
+    set_error("NULL buffer");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  contract_host(L_max, reinterpret_cast<const std::complex<double>*>(qhat),
+                reinterpret_cast<const std::complex<double>*>(khat), reinterpret_cast<std::complex<double>*>(uhat));
+  return CGCONV_OK;
+}
+
+}  // extern "C"

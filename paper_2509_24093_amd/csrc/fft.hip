@@ -1,0 +1,257 @@
+// Column DFT passes along the token axis for gfx950.
+//
+// The features are stored [batch][N][K][C] with channels fastest, so a
+// signal (fixed b, component, channel) runs down a column with stride K*C.
+// Each pass transforms R rows (R <= 256) of a tile of G adjacent columns:
+// every global access of a wavefront covers G consecutive columns of one row,
+// i.e. one contiguous segment of G*8 bytes (complex) or G*4 bytes (real), so
+// HBM reads and writes are coalesced without any transpose.  Inside a block
+// the length-R DFT is a two-stage Stockham factorisation R = R1 * R2: stage 1
+// reads its R1 inputs straight from HBM into registers and runs a radix-R1
+// DFT there, the R x G tile is exchanged once through LDS, stage 2 runs a
+// radix-R2 DFT in registers and writes straight to HBM.  Lengths above 256
+// use two passes (four-step factorisation, see the plan).
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace cgconv {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, -a.y * b.y), fmaf(a.x, b.y, a.y * b.x));
+}
+
+// exp(2 pi i k / 16) for k = 0..15 is (c16[k], s16[k]); forward DFTs use the
+// conjugate.  Used for the radix <= 16 register DFTs.
+__device__ __forceinline__ constexpr float c16(int k) {
+  constexpr float t[16] = {1.0f, 0.92387953251128674f, 0.70710678118654752f, 0.38268343236508977f,
+                           0.0f, -0.38268343236508977f, -0.70710678118654752f, -0.92387953251128674f,
+                           -1.0f, -0.92387953251128674f, -0.70710678118654752f, -0.38268343236508977f,
+                           0.0f, 0.38268343236508977f, 0.70710678118654752f, 0.92387953251128674f};
+  return t[k & 15];
+}
+__device__ __forceinline__ constexpr float s16(int k) { return c16(k - 4); }
+
+constexpr int bitrev(int x, int bits) {
+  int r = 0;
+  for (int i = 0; i < bits; ++i) r |= ((x >> i) & 1) << (bits - 1 - i);
+  return r;
+}
+constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
+
+// In-place DFT of R <= 16 values held in registers, natural order in and out:
+// X[f] = sum_e x[e] exp(DIR * 2 pi i e f / R).  Radix-2 decimation in time
+// with constant twiddles; multiplications by 1 and +-i are not emitted.
+template <int R, int DIR>
+__device__ __forceinline__ void dft_reg(float2 (&x)[R]) {
+  if constexpr (R == 1) {
+    return;
+  } else {
+    constexpr int B = ilog2(R);
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int r = bitrev(i, B);
+      if (r > i) {
+        const float2 t = x[i];
+        x[i] = x[r];
+        x[r] = t;
+      }
+    }
+#pragma unroll
+    for (int len = 2; len <= R; len <<= 1) {
+      const int half = len / 2;
+#pragma unroll
+      for (int i = 0; i < R; i += len) {
+#pragma unroll
+        for (int k = 0; k < half; ++k) {
+          const int tk = k * (16 / len);  // exp(DIR 2 pi i k / len) = w16^(DIR tk)
+          float2 b = x[i + k + half];
+          if (tk == 0) {
+          } else if (tk == 4) {
+            // multiply by DIR * i
+            b = DIR > 0 ? make_float2(-b.y, b.x) : make_float2(b.y, -b.x);
+          } else {
+            const float2 w = make_float2(c16(tk), DIR > 0 ? s16(tk) : -s16(tk));
+            b = cmul(b, w);
+          }
+          const float2 a = x[i + k];
+          x[i + k] = make_float2(a.x + b.x, a.y + b.y);
+          x[i + k + half] = make_float2(a.x - b.x, a.y - b.y);
+        }
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // quiet NaN
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;                   // round to nearest even
+}
+
+template <int INM>
+__device__ __forceinline__ float2 load_elem(const PassArgs& a, int b, long long row, int col) {
+  if constexpr (INM == IN_COMPLEX) {
+    const float2* p = static_cast<const float2*>(a.in0);
+    return p[b * a.in_bstride + row * a.W + col];
+  } else if constexpr (INM == IN_PAIR_F32) {
+    const long long i = b * a.in_bstride + row * a.W + col;
+    return make_float2(static_cast<const float*>(a.in0)[i], static_cast<const float*>(a.in1)[i]);
+  } else {
+    const long long i = b * a.in_bstride + row * a.W + col;
+    return make_float2(bf16_to_f32(static_cast<const uint16_t*>(a.in0)[i]),
+                       bf16_to_f32(static_cast<const uint16_t*>(a.in1)[i]));
+  }
+}
+
+template <int OUTM, int DIR>
+__device__ __forceinline__ void store_elem(const PassArgs& a, int b, int g, int f, int col, float2 v) {
+  if (a.inter) {
+    float2 w = a.tw[((long long)g * f) & a.Nmask];
+    if (DIR > 0) w.y = -w.y;
+    v = cmul(v, w);
+  }
+  v.x *= a.scale;
+  v.y *= a.scale;
+  const long long row = (long long)g * a.gs_out + (long long)f * a.fs_out;
+  if constexpr (OUTM == OUT_COMPLEX) {
+    static_cast<float2*>(a.out)[b * a.out_bstride + row * a.W + col] = v;
+  } else {
+    const int kk = col / a.Cp, cp = col - kk * a.Cp;
+    const long long base = b * a.out_bstride + row * a.KC + (long long)kk * a.C + 2 * cp;
+    const bool two = 2 * cp + 1 < a.C;
+    if constexpr (OUTM == OUT_SPLIT_F32) {
+      float* o = static_cast<float*>(a.out);
+      if (two && (a.C % 2 == 0)) {
+        *reinterpret_cast<float2*>(o + base) = v;
+      } else {
+        o[base] = v.x;
+        if (two) o[base + 1] = v.y;
+      }
+    } else {
+      uint16_t* o = static_cast<uint16_t*>(a.out);
+      const uint32_t lo = f32_to_bf16_bits(v.x), hi = f32_to_bf16_bits(v.y);
+      if (two && (a.C % 2 == 0)) {
+        *reinterpret_cast<uint32_t*>(o + base) = lo | (hi << 16);
+      } else {
+        o[base] = (uint16_t)lo;
+        if (two) o[base + 1] = (uint16_t)hi;
+      }
+    }
+  }
+}
+
+template <int R1, int R2, int G, int INM, int OUTM, int DIR>
+__global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
+  constexpr int R = R1 * R2;
+  __shared__ float2 lds[R2 > 1 ? R * G : 1];
+  const int col0 = blockIdx.x * G;
+  const int g = blockIdx.y;
+  const int b = blockIdx.z;
+
+  // stage 1: radix-R1 over inputs e = j1 + t*(R/R1)
+  for (int it = threadIdx.x; it < G * (R / R1); it += kThreads) {
+    const int cl = it % G, j1 = it / G;
+    const int col = col0 + cl;
+    const bool ok = col < a.W;
+    float2 x[R1];
+#pragma unroll
+    for (int t = 0; t < R1; ++t) {
+      const int e = j1 + t * (R / R1);
+      const long long row = (long long)g * a.gs_in + (long long)e * a.es_in;
+      x[t] = ok ? load_elem<INM>(a, b, row, col) : make_float2(0.f, 0.f);
+    }
+    dft_reg<R1, DIR>(x);
+    if constexpr (R2 == 1) {
+      if (ok) {
+#pragma unroll
+        for (int t = 0; t < R1; ++t) store_elem<OUTM, DIR>(a, b, g, t, col, x[t]);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < R1; ++t) lds[(j1 * R1 + t) * G + cl] = x[t];
+    }
+  }
+  if constexpr (R2 > 1) {
+    __syncthreads();
+    // stage 2: twiddle W_R^(j2 t), radix-R2, outputs f = j2 + t*R1
+    for (int it = threadIdx.x; it < G * (R / R2); it += kThreads) {
+      const int cl = it % G, j2 = it / G;
+      const int col = col0 + cl;
+      float2 x[R2];
+#pragma unroll
+      for (int t = 0; t < R2; ++t) {
+        x[t] = lds[(j2 + t * R1) * G + cl];
+        if (t > 0 && j2 > 0) {
+          float2 w = a.tw[((long long)j2 * t * a.tw_stride) & a.Nmask];
+          if (DIR > 0) w.y = -w.y;
+          x[t] = cmul(x[t], w);
+        }
+      }
+      dft_reg<R2, DIR>(x);
+      if (col < a.W) {
+#pragma unroll
+        for (int t = 0; t < R2; ++t) store_elem<OUTM, DIR>(a, b, g, j2 + t * R1, col, x[t]);
+      }
+    }
+  }
+}
+
+// Columns per block: R*G = 4096 elements (32 KB of LDS) for two-stage passes.
+template <int R>
+constexpr int tile_cols() {
+  return R <= 16 ? kThreads : 4096 / R;
+}
+
+template <int R, int INM, int OUTM, int DIR>
+hipError_t launch_r(const PassDesc& d, hipStream_t s) {
+  constexpr int R1 = R <= 16 ? R : 16;
+  constexpr int R2 = R / R1;
+  constexpr int G = tile_cols<R>();
+  const dim3 grid((d.a.W + G - 1) / G, d.groups, d.batch);
+  hipLaunchKernelGGL((fft_pass_kernel<R1, R2, G, INM, OUTM, DIR>), grid, dim3(kThreads), 0, s, d.a);
+  return hipGetLastError();
+}
+
+template <int INM, int OUTM, int DIR>
+hipError_t launch_modes(const PassDesc& d, hipStream_t s) {
+  switch (d.R) {
+    case 2: return launch_r<2, INM, OUTM, DIR>(d, s);
+    case 4: return launch_r<4, INM, OUTM, DIR>(d, s);
+    case 8: return launch_r<8, INM, OUTM, DIR>(d, s);
+    case 16: return launch_r<16, INM, OUTM, DIR>(d, s);
+    case 32: return launch_r<32, INM, OUTM, DIR>(d, s);
+    case 64: return launch_r<64, INM, OUTM, DIR>(d, s);
+    case 128: return launch_r<128, INM, OUTM, DIR>(d, s);
+    case 256: return launch_r<256, INM, OUTM, DIR>(d, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_fft_pass(const PassDesc& d, hipStream_t s) {
+  if (d.dir < 0) {
+    if (d.out_mode != OUT_COMPLEX) return hipErrorInvalidValue;
+    switch (d.in_mode) {
+      case IN_PAIR_F32: return launch_modes<IN_PAIR_F32, OUT_COMPLEX, -1>(d, s);
+      case IN_PAIR_BF16: return launch_modes<IN_PAIR_BF16, OUT_COMPLEX, -1>(d, s);
+      case IN_COMPLEX: return launch_modes<IN_COMPLEX, OUT_COMPLEX, -1>(d, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (d.in_mode != IN_COMPLEX) return hipErrorInvalidValue;
+  switch (d.out_mode) {
+    case OUT_COMPLEX: return launch_modes<IN_COMPLEX, OUT_COMPLEX, 1>(d, s);
+    case OUT_SPLIT_F32: return launch_modes<IN_COMPLEX, OUT_SPLIT_F32, 1>(d, s);
+    case OUT_SPLIT_BF16: return launch_modes<IN_COMPLEX, OUT_SPLIT_BF16, 1>(d, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace cgconv

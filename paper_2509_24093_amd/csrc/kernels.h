@@ -1,0 +1,85 @@
+// Internal interface between the plan (cgconv.cpp) and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace cgconv {
+
+// Input / output element modes of one column-DFT pass.
+enum InMode : int {
+  IN_COMPLEX = 0,   // float2 rows of width W
+  IN_PAIR_F32 = 1,  // z = q + i k from two fp32 arrays, rows of width W = K*C
+  IN_PAIR_BF16 = 2  // same, bfloat16 storage
+};
+enum OutMode : int {
+  OUT_COMPLEX = 0,   // float2 rows of width W
+  OUT_SPLIT_F32 = 1, // column (k, cp) -> out[k*C + 2cp] = re, out[k*C + 2cp + 1] = im (if < C)
+  OUT_SPLIT_BF16 = 2 // same, bfloat16 storage (round to nearest even)
+};
+
+// One pass of length-R DFTs along the token axis of a [batch][rows][W] array.
+// Block (tile, g, b) transforms, for columns tile*G .. tile*G+G-1, the R rows
+//   in_row(e)  = g*gs_in  + e*es_in,   e = 0..R-1
+// into the R rows
+//   out_row(f) = g*gs_out + f*fs_out,  f = 0..R-1,
+// X[f] = sum_e x[e] exp(dir * 2 pi i e f / R), then multiplies by the
+// inter-pass twiddle exp(dir * 2 pi i g f / N) if `inter` and by `scale`.
+struct PassArgs {
+  const void* in0;       // complex input, or q for pair input
+  const void* in1;       // k for pair input
+  void* out;
+  const float2* tw;      // tw[j] = exp(-2 pi i j / N), j = 0..N-1
+  long long in_bstride;  // elements (float2 or scalar) per batch entry of the input
+  long long out_bstride; // elements per batch entry of the output
+  int W;                 // complex columns per row
+  int C, Cp;             // channels, channel pairs (split output)
+  int KC;                // scalars per row of the split output: K*C
+  int gs_in, es_in, gs_out, fs_out;
+  int tw_stride;         // N / R
+  int Nmask;             // N - 1
+  int inter;             // 1: apply the inter-pass twiddle
+  float scale;
+};
+
+struct PassDesc {
+  int R;        // DFT length, power of two, 2..256
+  int in_mode;  // InMode
+  int out_mode; // OutMode
+  int dir;      // -1 forward, +1 inverse
+  int groups;   // number of g values
+  int batch;
+  PassArgs a;
+};
+
+hipError_t launch_fft_pass(const PassDesc& d, hipStream_t s);
+
+// Frequency-domain CG stage.  Z: full spectra of z = q + i k, [B][N][K][C]
+// float2.  W: spectra of out_c + i out_{c+1} (channel pairs), [B][N][K][Cp]
+// float2.  Every frequency pair (w, N-w), w = 0..N/2, is one point per channel.
+struct CgArgs {
+  const float2* Z;
+  float2* W;
+  float2* trash;    // K*Cp float2 after the real data of W: target of masked stores
+  long long N;
+  long long F;      // N/2 + 1
+  int K, C, Cp;
+  long long npts;   // B * F * 2Cp
+  // generic (table-driven) kernel only
+  const int* offs;       // [K+1] term offsets per complex-basis output index
+  const uint32_t* tkey;  // k1 | k2 << 8 | imag << 16
+  const float* tcoef;
+};
+
+hipError_t launch_cg(int L, const CgArgs& a, bool force_generic, hipStream_t s);
+
+// Launcher of the generated kernel for one L_max (explicitly specialised in
+// the translation unit built for that L).
+template <int L>
+hipError_t launch_cg_gen(const CgArgs& a, hipStream_t s);
+
+// Highest L_max with a generated, register-resident contraction body.
+int cg_generated_lmax();
+
+}  // namespace cgconv
