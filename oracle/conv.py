@@ -25,30 +25,41 @@ import numpy as np
 from .cg import dense_R, n_comp
 
 
-def _check(q, k, L):
-    q = np.asarray(q, dtype=np.float64)
-    k = np.asarray(k, dtype=np.float64)
+def _check(q, k, L, upcast=True):
+    q = np.asarray(q)
+    k = np.asarray(k)
     if q.shape != k.shape or q.ndim != 4:
         raise ValueError("q and k must both have shape (B, N, K, C)")
     if q.shape[2] != n_comp(L):
         raise ValueError(f"component axis must be (L+1)^2 = {n_comp(L)}")
+    if upcast:
+        q = q.astype(np.float64, copy=False)
+        k = k.astype(np.float64, copy=False)
     return q, k
 
 
 def _rows_direct(qb, kb, i_list, RK):
     """Direct token sum for one batch element and a list of output rows.
 
-    qb, kb: (N, K, C).  Returns (len(i_list), K, C).
+    qb, kb: (N, K, C), any float dtype; the sum runs in float64.
+    Returns (len(i_list), K, C).
+
+    P_i = sum_j q_j (x) k_{(i-j) mod N} = sum_m q_{(i-m) mod N} (x) k_m.  With
+    qr[t] = q[(-t) mod N] the first factor is qr[(m-i) mod N]; the sum over m
+    is taken in two contiguous ranges, m = i..N-1 (qr[0..N-1-i]) and
+    m = 0..i-1 (qr[N-i..N-1]), each as one matrix product.
     """
     N, K, C = qb.shape
-    j = np.arange(N)
-    qt = np.transpose(qb, (2, 1, 0))  # (C, K, N_j): q[j, a, c] as [c, a, j]
+    qrT = np.empty((C, K, N))                                   # qr as [c, a, t]
+    qrT[:, :, 0] = qb[0].T
+    qrT[:, :, 1:] = np.transpose(qb[:0:-1], (2, 1, 0))          # q[N-1], ..., q[1]
+    kT = np.ascontiguousarray(np.transpose(kb, (2, 0, 1)), dtype=np.float64)  # k as [c, m, b]
     out = np.empty((len(i_list), K, C))
     for n, i in enumerate(i_list):
-        ks = kb[(i - j) % N]                      # k_{(i-j) mod N}, (N_j, K, C)
-        ksc = np.transpose(ks, (2, 0, 1))         # (C, N_j, K)
-        P = np.matmul(qt, ksc)                    # (C, K_a, K_b): sum_j q_j (x) k_{i-j}
-        out[n] = (P.reshape(C, K * K) @ RK.T).T   # R_full : P_i for every channel
+        P = np.matmul(qrT[:, :, :N - i], kT[:, i:, :])          # m = i .. N-1
+        if i > 0:
+            P += np.matmul(qrT[:, :, N - i:], kT[:, :i, :])     # m = 0 .. i-1
+        out[n] = (P.reshape(C, K * K) @ RK.T).T                 # R_full : P_i for every channel
     return out
 
 
@@ -66,12 +77,15 @@ def cgconv_direct(q, k, L: int) -> np.ndarray:
 def cgconv_direct_rows(q, k, L: int, rows) -> np.ndarray:
     """Direct mode for selected output rows only; ``rows`` is a list of
     (b, i).  Returns (len(rows), K, C) float64."""
-    q, k = _check(q, k, L)
+    q, k = _check(q, k, L, upcast=False)
     B, N, K, C = q.shape
     RK = dense_R(L).reshape(K, K * K)
     out = np.empty((len(rows), K, C))
-    for n, (b, i) in enumerate(rows):
-        out[n] = _rows_direct(q[b], k[b], [i], RK)[0]
+    for b in sorted({b for b, _ in rows}):  # one batch element at a time
+        sel = [n for n, (bb, _) in enumerate(rows) if bb == b]
+        res = _rows_direct(q[b], k[b], [rows[n][1] for n in sel], RK)
+        for m, n in enumerate(sel):
+            out[n] = res[m]
     return out
 
 
@@ -79,11 +93,13 @@ def cgconv_fft(q, k, L: int, channels=None, freq_chunk: int = 4096) -> np.ndarra
     """FFT mode over the whole token axis; returns (B, N, K, C') float64 where
     C' = len(channels) if ``channels`` is given (channels are independent, so a
     subset is an exact check of those channels)."""
-    q, k = _check(q, k, L)
+    q, k = _check(q, k, L, upcast=False)
     if channels is not None:
         channels = list(channels)
         q = q[..., channels]
         k = k[..., channels]
+    q = q.astype(np.float64, copy=False)
+    k = k.astype(np.float64, copy=False)
     B, N, K, C = q.shape
     RK = dense_R(L).reshape(K, K * K)
     F = N // 2 + 1
