@@ -101,17 +101,28 @@ def cpu_baseline(q, k, L, budget_s, got):
         blas_threads = None
     B, N = q.shape[0], q.shape[1]
     rng = np.random.default_rng(2024)
-    rows = [(0, 0), (B - 1, N - 1)] + [(int(rng.integers(B)), int(rng.integers(N))) for _ in range(254)]
+    # rows in chunks of 8 per batch element, cycling over b, until the budget
+    # is spent; (0, 0) and (B-1, N-1) are always included
+    rows, ref = [], []
     t0 = time.perf_counter()
-    cgconv_direct_rows(q, k, L, rows[:1])
-    t1 = time.perf_counter()
-    per_row = t1 - t0
-    R = int(max(2, min(len(rows), budget_s / max(per_row, 1e-6))))
-    t0 = time.perf_counter()
-    ref = cgconv_direct_rows(q, k, L, rows[:R])
+    chunk = 0
+    while True:
+        b = chunk % B
+        picks = [int(x) for x in rng.integers(0, N, size=8)]
+        if chunk == 0:
+            picks[0] = 0
+        if chunk == B - 1:
+            picks[0] = N - 1
+        part = [(b, i) for i in picks]
+        ref.extend(cgconv_direct_rows(q, k, L, part))
+        rows.extend(part)
+        chunk += 1
+        if time.perf_counter() - t0 >= budget_s and chunk >= B:
+            break
     dt = time.perf_counter() - t0
+    R = len(rows)
     num = den = 0.0
-    for n, (b, i) in enumerate(rows[:R]):
+    for n, (b, i) in enumerate(rows):
         d = got[b, i].astype(np.float64) - ref[n]
         num += float((d * d).sum())
         den += float((ref[n] * ref[n]).sum())
