@@ -12,8 +12,15 @@ namespace cgdev {
 
 namespace {
 
+// Waves per SIMD the register allocation must allow.  Up to L_max = 6 the
+// inputs (2K complex values) fit a 256-register budget with at most a few
+// spills, and a second wave per SIMD hides the load latency of the first
+// (measured: 1.89 -> 1.26 ms at L_max = 6); L_max = 7, 8 need the whole
+// 512-entry file of one wave.
+constexpr int kMinWavesPerSimd = CGCONV_TU_L <= 6 ? 2 : 1;
+
 template <int L>
-__global__ __launch_bounds__(cgdev::kCgThreads) void cg_gen_kernel(CgArgs a) {
+__global__ __launch_bounds__(cgdev::kCgThreads, kMinWavesPerSimd) void cg_gen_kernel(CgArgs a) {
   using namespace cgdev;
   constexpr int K = (L + 1) * (L + 1);
   const long long p = (long long)blockIdx.x * kCgThreads + threadIdx.x;

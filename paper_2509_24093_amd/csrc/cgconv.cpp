@@ -21,7 +21,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/cgconv.h"
+#include "cgconv.h"
 #include "cg_table.h"
 #include "kernels.h"
 

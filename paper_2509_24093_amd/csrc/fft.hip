@@ -109,13 +109,12 @@ __device__ __forceinline__ float2 load_elem(const PassArgs& a, int b, long long 
   }
 }
 
-template <int OUTM, int DIR>
-__device__ __forceinline__ void store_elem(const PassArgs& a, int b, int g, int f, int col, float2 v) {
-  if (a.inter) {
-    float2 w = a.tw[((long long)g * f) & a.Nmask];
-    if (DIR > 0) w.y = -w.y;
-    v = cmul(v, w);
-  }
+// Store one output element after the inter-pass twiddle (tw_pass[f] =
+// exp(dir 2 pi i g f / N), staged in LDS) and the scale.
+template <int OUTM>
+__device__ __forceinline__ void store_elem(const PassArgs& a, int b, int g, int f, int col, float2 v,
+                                           const float2* tw_pass) {
+  if (a.inter) v = cmul(v, tw_pass[f]);
   v.x *= a.scale;
   v.y *= a.scale;
   const long long row = (long long)g * a.gs_out + (long long)f * a.fs_out;
@@ -150,9 +149,28 @@ template <int R1, int R2, int G, int INM, int OUTM, int DIR>
 __global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
   constexpr int R = R1 * R2;
   __shared__ float2 lds[R2 > 1 ? R * G : 1];
+  __shared__ float2 tw_int[R2 > 1 ? R : 1];  // exp(dir 2 pi i x / R), x < R
+  __shared__ float2 tw_pass[R];               // exp(dir 2 pi i g f / N), f < R
   const int col0 = blockIdx.x * G;
   const int g = blockIdx.y;
   const int b = blockIdx.z;
+
+  // twiddle tables of this block, read once from the global table
+  for (int x = threadIdx.x; x < R; x += kThreads) {
+    if constexpr (R2 > 1) {
+      float2 w = a.tw[((long long)x * a.tw_stride) & a.Nmask];
+      if (DIR > 0) w.y = -w.y;
+      tw_int[x] = w;
+    }
+    if (a.inter) {
+      float2 w = a.tw[((long long)g * x) & a.Nmask];
+      if (DIR > 0) w.y = -w.y;
+      tw_pass[x] = w;
+    }
+  }
+  if constexpr (R2 == 1) {
+    if (a.inter) __syncthreads();  // uniform over the block; stage 1 stores use tw_pass
+  }
 
   // stage 1: radix-R1 over inputs e = j1 + t*(R/R1)
   for (int it = threadIdx.x; it < G * (R / R1); it += kThreads) {
@@ -170,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
     if constexpr (R2 == 1) {
       if (ok) {
 #pragma unroll
-        for (int t = 0; t < R1; ++t) store_elem<OUTM, DIR>(a, b, g, t, col, x[t]);
+        for (int t = 0; t < R1; ++t) store_elem<OUTM>(a, b, g, t, col, x[t], tw_pass);
       }
     } else {
 #pragma unroll
@@ -187,16 +205,12 @@ __global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
 #pragma unroll
       for (int t = 0; t < R2; ++t) {
         x[t] = lds[(j2 + t * R1) * G + cl];
-        if (t > 0 && j2 > 0) {
-          float2 w = a.tw[((long long)j2 * t * a.tw_stride) & a.Nmask];
-          if (DIR > 0) w.y = -w.y;
-          x[t] = cmul(x[t], w);
-        }
+        if (t > 0 && j2 > 0) x[t] = cmul(x[t], tw_int[j2 * t]);  // W_R^(j2 t), j2 t < R
       }
       dft_reg<R2, DIR>(x);
       if (col < a.W) {
 #pragma unroll
-        for (int t = 0; t < R2; ++t) store_elem<OUTM, DIR>(a, b, g, j2 + t * R1, col, x[t]);
+        for (int t = 0; t < R2; ++t) store_elem<OUTM>(a, b, g, j2 + t * R1, col, x[t], tw_pass);
       }
     }
   }
