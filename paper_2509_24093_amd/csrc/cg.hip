@@ -39,8 +39,8 @@ __global__ __launch_bounds__(kGenThreads) void cg_generic_kernel(CgArgs a) {
   {
     const bool cv = pt.valid && pt.c < a.C;
     const long long wn = (a.N - pt.w) & (a.N - 1);
-    const float2* za = a.Z + ((pt.b * a.N + pt.w) * K) * a.C + pt.c;
-    const float2* zb = a.Z + ((pt.b * a.N + wn) * K) * a.C + pt.c;
+    const float2* za = a.Z + ((pt.b * a.N + freq_row(pt.w, a)) * K) * a.C + pt.c;
+    const float2* zb = a.Z + ((pt.b * a.N + freq_row(wn, a)) * K) * a.C + pt.c;
     for (int k = 0; k < K; ++k) {
       const float2 A = cv ? za[(long long)k * a.C] : make_float2(0.f, 0.f);
       const float2 B = cv ? zb[(long long)k * a.C] : make_float2(0.f, 0.f);

@@ -53,6 +53,11 @@ struct Point {
   bool valid;
 };
 
+// storage row of frequency w (see CgArgs)
+__device__ __forceinline__ long long freq_row(long long w, const CgArgs& a) {
+  return ((w & ((1LL << a.n1_log2) - 1)) << a.n2_log2) | (w >> a.n1_log2);
+}
+
 __device__ __forceinline__ Point point_of(long long p, const CgArgs& a) {
   Point pt;
   pt.valid = p < a.npts;
@@ -72,8 +77,8 @@ __device__ __forceinline__ void load_unpack(const CgArgs& a, const Point& pt, Ar
   const bool cv = pt.valid && pt.c < a.C;
   const long long wn = (a.N - pt.w) & (a.N - 1);
   const int cl = pt.c < a.C ? pt.c : a.C - 1;  // the padding channel of odd C loads a real one, then zeroes it
-  const float2* za = a.Z + ((pt.b * a.N + pt.w) * K) * a.C + cl;
-  const float2* zb = a.Z + ((pt.b * a.N + wn) * K) * a.C + cl;
+  const float2* za = a.Z + ((pt.b * a.N + freq_row(pt.w, a)) * K) * a.C + cl;
+  const float2* zb = a.Z + ((pt.b * a.N + freq_row(wn, a)) * K) * a.C + cl;
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     // every lane's address is valid (out-of-range points alias point 0):
@@ -111,7 +116,7 @@ __device__ __forceinline__ PairStore make_store(const CgArgs& a, const Point& pt
   st.Cp = a.Cp;
   st.even = (pt.c & 1) == 0;
   const bool write = pt.valid && (st.even || (wn != pt.w));
-  const long long row = st.even ? pt.w : wn;
+  const long long row = freq_row(st.even ? pt.w : wn, a);
   float2* real = a.W + ((pt.b * a.N + row) * K) * a.Cp + (pt.c >> 1);
   st.dst = write ? real : a.trash + (pt.c >> 1);
   return st;

@@ -6,6 +6,8 @@
 //              w = w1 + N1 w2:
 //     F1  for each n2: length-N1 DFT over n1, twiddle W_N^(n2 w1)   q,k -> Y
 //     F2  for each w1: length-N2 DFT over n2                         Y -> Z
+//         (Z, W keep frequency w1 + N1 w2 at row w1 N2 + w2, so F2 and I1
+//          read and write contiguous row blocks)
 //     CG  sparse tensor product per frequency pair and channel       Z -> W
 //     I1  for each w1: inverse length-N2 DFT, twiddle W_N^(-n2 w1)   W -> V
 //     I2  for each n2: inverse length-N1 DFT, x 1/N, split channels  V -> out
@@ -154,6 +156,8 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
   ca.offs = p->d_offs;
   ca.tkey = p->d_tkey;
   ca.tcoef = p->d_tcoef;
+  ca.n1_log2 = ilog2(p->N1 ? p->N1 : p->N);
+  ca.n2_log2 = ilog2(p->N1 ? p->N2 : 1);
   const long long N = p->N;
   const float inv_n = 1.0f / (float)N;
   hipEvent_t* ev = nullptr;  // events of this call if it is timed
@@ -186,7 +190,8 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
     if (e != hipSuccess) goto fail;
     mark();
-    e = pass(N2, IN_COMPLEX, OUT_COMPLEX, -1, N1, p->ws1, nullptr, p->ws2, N * Wz, N * Wz, (int)Wz, N2, 1, 1, N1, 0,
+    // frequency w1 + N1 w2 goes to row w1 N2 + w2 (contiguous per block, see CgArgs)
+    e = pass(N2, IN_COMPLEX, OUT_COMPLEX, -1, N1, p->ws1, nullptr, p->ws2, N * Wz, N * Wz, (int)Wz, N2, 1, N2, 1, 0,
              1.0f);
     if (e != hipSuccess) goto fail;
     mark();
@@ -196,7 +201,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     e = launch_cg(p->L, ca, p->force_generic, s);
     if (e != hipSuccess) goto fail;
     mark();
-    e = pass(N2, IN_COMPLEX, OUT_COMPLEX, 1, N1, p->ws1, nullptr, p->ws2, N * Ww, N * Ww, (int)Ww, 1, N1, N2, 1, 1,
+    e = pass(N2, IN_COMPLEX, OUT_COMPLEX, 1, N1, p->ws1, nullptr, p->ws2, N * Ww, N * Ww, (int)Ww, N2, 1, N2, 1, 1,
              1.0f);
     if (e != hipSuccess) goto fail;
     mark();

@@ -58,11 +58,15 @@ hipError_t launch_fft_pass(const PassDesc& d, hipStream_t s);
 // Frequency-domain CG stage.  Z: full spectra of z = q + i k, [B][N][K][C]
 // float2.  W: spectra of out_c + i out_{c+1} (channel pairs), [B][N][K][Cp]
 // float2.  Every frequency pair (w, N-w), w = 0..N/2, is one point per channel.
+// Frequency w is stored at row pos(w) = (w mod N1) * N2 + w / N1 of Z and W
+// (N1 = N, N2 = 1 for single-pass transforms), so that the DFT passes on
+// either side of this stage read and write contiguous row blocks.
 struct CgArgs {
   const float2* Z;
   float2* W;
   float2* trash;    // K*Cp float2 after the real data of W: target of masked stores
   long long N;
+  int n1_log2, n2_log2;
   long long F;      // N/2 + 1
   int K, C, Cp;
   long long npts;   // B * F * 2Cp
