@@ -45,6 +45,7 @@ struct PairStore {
     const float2 out = even ? make_float2(u.x - v.y, u.y + v.x) : make_float2(v.x + u.y, u.x - v.y);
     dst[(long long)kout * Cp] = out;
   }
+  __device__ __forceinline__ void end_phase(int) const {}
 };
 
 struct Point {
@@ -70,6 +71,26 @@ __device__ __forceinline__ Point point_of(long long p, const CgArgs& a) {
   return pt;
 }
 
+// Real basis (l, +mu) = c, (l, -mu) = s  ->  complex-m basis, in place:
+//   a[l,-mu] = x_c + i x_s,  a[l,+mu] = x_c - i x_s.
+template <int K, class Arr>
+__device__ __forceinline__ void to_complex_basis(Arr& qa, Arr& ka) {
+#pragma unroll
+  for (int l = 1; l * l < K; ++l) {
+#pragma unroll
+    for (int mu = 1; mu <= l; ++mu) {
+      const int c = l * l + l + mu, s = l * l + l - mu;
+      float2 xc = qa[c], xs = qa[s];
+      qa[s] = make_float2(xc.x - xs.y, xc.y + xs.x);
+      qa[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
+      xc = ka[c];
+      xs = ka[s];
+      ka[s] = make_float2(xc.x - xs.y, xc.y + xs.x);
+      ka[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
+    }
+  }
+}
+
 // Load both spectra at (w, N-w) for all K components and form 2Q, 2K in the
 // complex-m basis (qa, ka).
 template <int K, class Arr>
@@ -92,22 +113,7 @@ __device__ __forceinline__ void load_unpack(const CgArgs& a, const Point& pt, Ar
     qa[k] = make_float2(A.x + B.x, A.y - B.y);  // A + conj B      = 2Q
     ka[k] = make_float2(A.y + B.y, B.x - A.x);  // -i (A - conj B)  = 2K
   }
-  // real basis (l, +mu) = c, (l, -mu) = s  ->  complex-m basis:
-  //   a[l,-mu] = x_c + i x_s,  a[l,+mu] = x_c - i x_s
-#pragma unroll
-  for (int l = 1; l * l < K; ++l) {
-#pragma unroll
-    for (int mu = 1; mu <= l; ++mu) {
-      const int c = l * l + l + mu, s = l * l + l - mu;
-      float2 xc = qa[c], xs = qa[s];
-      qa[s] = make_float2(xc.x - xs.y, xc.y + xs.x);
-      qa[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
-      xc = ka[c];
-      xs = ka[s];
-      ka[s] = make_float2(xc.x - xs.y, xc.y + xs.x);
-      ka[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
-    }
-  }
+  to_complex_basis<K>(qa, ka);
 }
 
 __device__ __forceinline__ PairStore make_store(const CgArgs& a, const Point& pt, int K) {

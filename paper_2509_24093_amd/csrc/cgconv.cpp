@@ -12,8 +12,11 @@
 //     I1  for each w1: inverse length-N2 DFT, twiddle W_N^(-n2 w1)   W -> V
 //     I2  for each n2: inverse length-N1 DFT, x 1/N, split channels  V -> out
 // Y, Z, W, V live in two plan-owned workspaces of B*N*K*C float2 each.
+//   512 <= N <= 16384, L_max <= 6: N2 = 64 and F2 + CG + I1 run as one fused
+//   kernel (cg_fused.hip) between F1 and I2; the spectra stay on chip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <complex>
 #include <cstdarg>
@@ -55,6 +58,7 @@ struct cgconv_plan {
   int64_t B = 0, N = 0, C = 0, Cp = 0;
   int L = 0, K = 0;
   int64_t N1 = 0, N2 = 0;  // N1 == 0: single pass
+  bool fused = false;      // two-pass with N2 = 64 and the fused middle kernel
   int device = 0;
   int64_t nnz = 0, paths = 0, products = 0;
   size_t ws_bytes = 0;
@@ -91,6 +95,20 @@ void free_plan(cgconv_plan* p) {
 
 const char* const kStages2[] = {"fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"};
 const char* const kStages1[] = {"fft_fwd", "cg", "fft_inv"};
+const char* const kStagesF[] = {"fft_fwd_1", "cg_fused", "fft_inv_2"};
+
+hipError_t launch_fused(int L, const FusedArgs& a, hipStream_t s) {
+  switch (L) {
+    case 0: return launch_cg_fused<0>(a, s);
+    case 1: return launch_cg_fused<1>(a, s);
+    case 2: return launch_cg_fused<2>(a, s);
+    case 3: return launch_cg_fused<3>(a, s);
+    case 4: return launch_cg_fused<4>(a, s);
+    case 5: return launch_cg_fused<5>(a, s);
+    case 6: return launch_cg_fused<6>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
@@ -171,7 +189,32 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     ++stage;
   };
   mark();
-  if (p->N1 == 0) {
+  if (p->fused) {
+    // F1 (Y rows w1*64 + n2) -> fused F2 + CG + I1 (V rows w1*64 + n2) -> I2
+    const int N1 = (int)p->N1, N2 = 64;
+    e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
+    if (e != hipSuccess) goto fail;
+    mark();
+    FusedArgs fa;
+    fa.Y = p->ws1;
+    fa.V = p->ws2;
+    fa.vtrash = p->ws2 + p->B * N * K * p->Cp;
+    fa.tw = p->tw;
+    fa.N = N;
+    fa.N1 = N1;
+    fa.units = N1 / 2 + 1;
+    fa.B = (int)p->B;
+    fa.C = (int)p->C;
+    fa.Cp = (int)p->Cp;
+    fa.Cb = (int)((p->C + 3) / 4);
+    e = launch_fused(p->L, fa, s);
+    if (e != hipSuccess) goto fail;
+    mark();
+    e = pass(N1, IN_COMPLEX, out_split, 1, N2, p->ws2, nullptr, out, N * Ww, N * K * p->C, (int)Ww, 1, N2, 1, N2, 0,
+             inv_n);
+    if (e != hipSuccess) goto fail;
+    mark();
+  } else if (p->N1 == 0) {
     e = pass((int)N, in_pair, OUT_COMPLEX, -1, 1, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 0, 1, 0, 1, 0, 1.0f);
     if (e != hipSuccess) goto fail;
     mark();
@@ -285,13 +328,18 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
   p->Cp = Cp;
   p->L = L_max;
   p->K = K;
-  if (N > 256) {
+  if (const char* env = std::getenv("CGCONV_FORCE_GENERIC")) p->force_generic = env[0] == '1';
+  const char* unfused = std::getenv("CGCONV_UNFUSED");
+  if (N >= 512 && N <= 16384 && L_max <= kFusedLmax && !(unfused && unfused[0] == '1') && !p->force_generic) {
+    p->fused = true;
+    p->N2 = 64;
+    p->N1 = N / 64;
+  } else if (N > 256) {
     const int lg = ilog2(N);
     p->N1 = int64_t(1) << ((lg + 1) / 2);
     p->N2 = N / p->N1;
   }
-  p->n_stages = p->N1 ? 5 : 3;
-  if (const char* env = std::getenv("CGCONV_FORCE_GENERIC")) p->force_generic = env[0] == '1';
+  p->n_stages = (p->N1 && !p->fused) ? 5 : 3;
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) {
     set_error("hipGetDevice failed: %s", hipGetErrorString(e));
@@ -330,8 +378,9 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
   }
   p->paths = n_paths(L_max);
   // each workspace holds a [B][N][K][C] float2 array, followed by a trash area
-  // of K*Cp float2 that absorbs the masked stores of the CG stage
-  const size_t ws = ((size_t)batch * N * K * C + (size_t)K * Cp) * sizeof(float2);
+  // that absorbs the masked stores of the CG stage (K*Cp float2, at least 256)
+  const size_t trash = std::max<size_t>((size_t)K * Cp, 256);
+  const size_t ws = ((size_t)batch * N * K * C + trash) * sizeof(float2);
   p->ws_bytes = 2 * ws;
   if (const char* env = std::getenv("CGCONV_TEST_FAIL_ALLOC"); env && env[0] == '1') {
     set_error("workspace allocation of %zu bytes failed (forced by CGCONV_TEST_FAIL_ALLOC)", p->ws_bytes);
@@ -425,6 +474,7 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
 
 const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
   if (!plan || stage < 0 || stage >= plan->n_stages) return "";
+  if (plan->fused) return kStagesF[stage];
   return plan->N1 ? kStages2[stage] : kStages1[stage];
 }
 

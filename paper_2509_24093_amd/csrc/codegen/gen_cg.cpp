@@ -15,6 +15,8 @@
 //                 per (J) coefficient;
 //   key form:     t_J = sum_l2 coef * ka[l2,m2] (2 FMAs per coefficient),
 //                 then w[J] += qa[l1,m1] * t_J (4 FMAs per J).
+// Every output component is handed to st(k, value) as soon as it is final;
+// st.end_phase(mu) follows the last component of phase mu.
 // Coefficients are emitted as float literals (the double value rounded to
 // nearest float).  The one subtraction of every complex product goes through
 // fnma() (c - a*b as a single v_fma_f32 with a negated operand, see
@@ -179,6 +181,7 @@ void emit_body(FILE* f, int L, long* ops_out) {
       }
     }
     e.inited.clear();
+    std::fprintf(f, "      st.end_phase(%d);\n", mu);
     std::fprintf(f, "    }\n");
   }
   std::fprintf(f, "  }\n");

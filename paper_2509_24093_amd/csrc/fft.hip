@@ -13,78 +13,16 @@
 // use two passes (four-step factorisation, see the plan).
 #include <hip/hip_runtime.h>
 
+#include "fft_reg.h"
 #include "kernels.h"
 
 namespace cgconv {
 namespace {
 
+using dft::cmul;
+using dft::dft_reg;
+
 constexpr int kThreads = 256;
-
-__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
-  return make_float2(fmaf(a.x, b.x, -a.y * b.y), fmaf(a.x, b.y, a.y * b.x));
-}
-
-// exp(2 pi i k / 16) for k = 0..15 is (c16[k], s16[k]); forward DFTs use the
-// conjugate.  Used for the radix <= 16 register DFTs.
-__device__ __forceinline__ constexpr float c16(int k) {
-  constexpr float t[16] = {1.0f, 0.92387953251128674f, 0.70710678118654752f, 0.38268343236508977f,
-                           0.0f, -0.38268343236508977f, -0.70710678118654752f, -0.92387953251128674f,
-                           -1.0f, -0.92387953251128674f, -0.70710678118654752f, -0.38268343236508977f,
-                           0.0f, 0.38268343236508977f, 0.70710678118654752f, 0.92387953251128674f};
-  return t[k & 15];
-}
-__device__ __forceinline__ constexpr float s16(int k) { return c16(k - 4); }
-
-constexpr int bitrev(int x, int bits) {
-  int r = 0;
-  for (int i = 0; i < bits; ++i) r |= ((x >> i) & 1) << (bits - 1 - i);
-  return r;
-}
-constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
-
-// In-place DFT of R <= 16 values held in registers, natural order in and out:
-// X[f] = sum_e x[e] exp(DIR * 2 pi i e f / R).  Radix-2 decimation in time
-// with constant twiddles; multiplications by 1 and +-i are not emitted.
-template <int R, int DIR>
-__device__ __forceinline__ void dft_reg(float2 (&x)[R]) {
-  if constexpr (R == 1) {
-    return;
-  } else {
-    constexpr int B = ilog2(R);
-#pragma unroll
-    for (int i = 0; i < R; ++i) {
-      const int r = bitrev(i, B);
-      if (r > i) {
-        const float2 t = x[i];
-        x[i] = x[r];
-        x[r] = t;
-      }
-    }
-#pragma unroll
-    for (int len = 2; len <= R; len <<= 1) {
-      const int half = len / 2;
-#pragma unroll
-      for (int i = 0; i < R; i += len) {
-#pragma unroll
-        for (int k = 0; k < half; ++k) {
-          const int tk = k * (16 / len);  // exp(DIR 2 pi i k / len) = w16^(DIR tk)
-          float2 b = x[i + k + half];
-          if (tk == 0) {
-          } else if (tk == 4) {
-            // multiply by DIR * i
-            b = DIR > 0 ? make_float2(-b.y, b.x) : make_float2(b.y, -b.x);
-          } else {
-            const float2 w = make_float2(c16(tk), DIR > 0 ? s16(tk) : -s16(tk));
-            b = cmul(b, w);
-          }
-          const float2 a = x[i + k];
-          x[i + k] = make_float2(a.x + b.x, a.y + b.y);
-          x[i + k + half] = make_float2(a.x - b.x, a.y - b.y);
-        }
-      }
-    }
-  }
-}
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
@@ -145,8 +83,8 @@ __device__ __forceinline__ void store_elem(const PassArgs& a, int b, int g, int 
   }
 }
 
-template <int R1, int R2, int G, int INM, int OUTM, int DIR>
-__global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
+template <int R1, int R2, int G, int T, int INM, int OUTM, int DIR>
+__global__ __launch_bounds__(T) void fft_pass_kernel(PassArgs a) {
   constexpr int R = R1 * R2;
   __shared__ float2 lds[R2 > 1 ? R * G : 1];
   __shared__ float2 tw_int[R2 > 1 ? R : 1];  // exp(dir 2 pi i x / R), x < R
@@ -156,7 +94,7 @@ __global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
   const int b = blockIdx.z;
 
   // twiddle tables of this block, read once from the global table
-  for (int x = threadIdx.x; x < R; x += kThreads) {
+  for (int x = threadIdx.x; x < R; x += T) {
     if constexpr (R2 > 1) {
       float2 w = a.tw[((long long)x * a.tw_stride) & a.Nmask];
       if (DIR > 0) w.y = -w.y;
@@ -173,7 +111,7 @@ __global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
   }
 
   // stage 1: radix-R1 over inputs e = j1 + t*(R/R1)
-  for (int it = threadIdx.x; it < G * (R / R1); it += kThreads) {
+  for (int it = threadIdx.x; it < G * (R / R1); it += T) {
     const int cl = it % G, j1 = it / G;
     const int col = col0 + cl;
     const bool ok = col < a.W;
@@ -198,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
   if constexpr (R2 > 1) {
     __syncthreads();
     // stage 2: twiddle W_R^(j2 t), radix-R2, outputs f = j2 + t*R1
-    for (int it = threadIdx.x; it < G * (R / R2); it += kThreads) {
+    for (int it = threadIdx.x; it < G * (R / R2); it += T) {
       const int cl = it % G, j2 = it / G;
       const int col = col0 + cl;
       float2 x[R2];
@@ -216,19 +154,28 @@ __global__ __launch_bounds__(kThreads) void fft_pass_kernel(PassArgs a) {
   }
 }
 
-// Columns per block: R*G = 4096 elements (32 KB of LDS) for two-stage passes.
-template <int R>
+// Columns per block and threads: R*G = 4096 elements (32 KB of LDS) for
+// two-stage passes up to R = 128.  R = 256 keeps wide rows instead: 32
+// complex columns (256 B) with 512 threads and 64 KB, and for the real pair
+// input 64 columns (256 B of q and of k per row) with 1024 threads and
+// 128 KB (measured at the point-cloud shape: 0.95 -> 0.66 ms).
+template <int R, int INM>
 constexpr int tile_cols() {
-  return R <= 16 ? kThreads : 4096 / R;
+  return R <= 16 ? kThreads : (R == 256 ? (INM == IN_COMPLEX ? 32 : 64) : 4096 / R);
+}
+template <int R, int INM>
+constexpr int tile_threads() {
+  return R == 256 ? (INM == IN_COMPLEX ? 512 : 1024) : kThreads;
 }
 
 template <int R, int INM, int OUTM, int DIR>
 hipError_t launch_r(const PassDesc& d, hipStream_t s) {
   constexpr int R1 = R <= 16 ? R : 16;
   constexpr int R2 = R / R1;
-  constexpr int G = tile_cols<R>();
+  constexpr int G = tile_cols<R, INM>();
+  constexpr int T = tile_threads<R, INM>();
   const dim3 grid((d.a.W + G - 1) / G, d.groups, d.batch);
-  hipLaunchKernelGGL((fft_pass_kernel<R1, R2, G, INM, OUTM, DIR>), grid, dim3(kThreads), 0, s, d.a);
+  hipLaunchKernelGGL((fft_pass_kernel<R1, R2, G, T, INM, OUTM, DIR>), grid, dim3(T), 0, s, d.a);
   return hipGetLastError();
 }
 

@@ -83,7 +83,29 @@ hipError_t launch_cg(int L, const CgArgs& a, bool force_generic, hipStream_t s);
 template <int L>
 hipError_t launch_cg_gen(const CgArgs& a, hipStream_t s);
 
+// Fused second forward pass + CG stage + first inverse pass for two-pass
+// plans with N2 = 64 (see cg_fused.hip).  Y: output of the first forward
+// pass, class w1 at rows w1*64 + n2; V: input of the last inverse pass,
+// [B][N][K][Cp] float2, same row order.
+struct FusedArgs {
+  const float2* Y;
+  float2* V;
+  float2* vtrash;    // >= 256 float2: target of masked stores
+  const float2* tw;  // exp(-2 pi i j / N)
+  long long N;
+  int N1;            // N / 64
+  int units;         // N1/2 + 1 class pairs per batch element
+  int B, C, Cp;
+  int Cb;            // channel blocks of 4
+};
+
+template <int L>
+hipError_t launch_cg_fused(const FusedArgs& a, hipStream_t s);
+
 // Highest L_max with a generated, register-resident contraction body.
 int cg_generated_lmax();
+
+// Highest L_max with a fused kernel.
+constexpr int kFusedLmax = 6;
 
 }  // namespace cgconv
