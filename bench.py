@@ -42,7 +42,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 VALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 VALU_PEAK_PACKED_TFLOPS = 157.3
 METRIC = "CG-conv tokens/sec at N=16384, L_max=6, C=32; achieved HBM GB/s vs peak"
-CG_SOURCES = ["paper_2509_24093_amd/csrc/cg_gen.hip", "paper_2509_24093_amd/csrc/cg_common.h",
+CG_SOURCES = ["paper_2509_24093_amd/csrc/cg_gen.hip", "paper_2509_24093_amd/csrc/cg_fused.hip",
+              "paper_2509_24093_amd/csrc/cg_common.h", "paper_2509_24093_amd/csrc/fft_reg.h",
               "paper_2509_24093_amd/csrc/codegen/gen_cg.cpp", "paper_2509_24093_amd/csrc/cg_table.cpp",
               "paper_2509_24093_amd/csrc/kernels.h"]
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "cg_kernel_pointcloud_pmc.md")
@@ -60,9 +61,10 @@ def cg_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def committed_traffic(workload):
-    """HBM bytes per CG launch from the committed rocprofv3 counter summary,
-    if it was taken on the current CG kernel source and this workload."""
+def committed_counters(workload):
+    """The committed rocprofv3 counter summary (calibrated HBM bytes per CG
+    launch and per whole step) if it was taken on the current CG kernel
+    source and this workload, else (None, reason)."""
     if not os.path.exists(PMC_SUMMARY):
         return None, "no counter summary committed"
     text = open(PMC_SUMMARY).read()
@@ -75,7 +77,7 @@ def committed_traffic(workload):
         return None, "CG kernel changed since the counters were taken"
     if d.get("workload") != workload:
         return None, "counters were taken on another workload"
-    return d["cg_hbm_bytes_per_launch"], "rocprofv3 FETCH_SIZE+WRITE_SIZE, copy-calibrated"
+    return d, "rocprofv3 FETCH_SIZE+WRITE_SIZE, copy-calibrated"
 
 
 def copy_calibration():
@@ -202,19 +204,36 @@ def main():
     Sc = B * N * K * C * 4
     Cp = (C + 1) // 2
     Sp = B * N * K * Cp * 8
-    io = ({"fft_fwd_1": 2 * S + 2 * Sc, "fft_fwd_2": 4 * Sc, "cg": 2 * Sc + Sp, "fft_inv_1": 2 * Sp,
-           "fft_inv_2": Sp + S} if N > 256 else
-          {"fft_fwd": 2 * S + 2 * Sc, "cg": 2 * Sc + Sp, "fft_inv": Sp + S})
+    if "cg_fused" in stage_avg:
+        io = {"fft_fwd_1": 2 * S + 2 * Sc, "cg_fused": 2 * Sc + Sp, "fft_inv_2": Sp + S}
+    elif N > 256:
+        io = {"fft_fwd_1": 2 * S + 2 * Sc, "fft_fwd_2": 4 * Sc, "cg": 2 * Sc + Sp, "fft_inv_1": 2 * Sp,
+              "fft_inv_2": Sp + S}
+    else:
+        io = {"fft_fwd": 2 * S + 2 * Sc, "cg": 2 * Sc + Sp, "fft_inv": Sp + S}
     stages = {s: {"ms": round(t, 4), "bytes": io.get(s), "gbs": round(io.get(s, 0) / (t * 1e-3) / 1e9, 1)}
               for s, t in stage_avg.items()}
     F = N // 2 + 1
     points = B * F * C
     cg_flops_per_point = 6 * n_products + 4 * nnz
-    cg_ms = stage_avg["cg"]
-    achieved_tflops = points * cg_flops_per_point / (cg_ms * 1e-3) / 1e12
-    traffic, traffic_src = committed_traffic(args.workload) if not args.bf16 else (None, "bf16 run")
+    dom = "cg_fused" if "cg_fused" in stage_avg else "cg"
+    cg_ms = stage_avg[dom]
+    flops = points * cg_flops_per_point
+    flop_model = (f"(6*{n_products} distinct complex products + 4*{nnz} non-zeros) per "
+                  f"(b, frequency 0..N/2, channel) point, {points} points")
+    if dom == "cg_fused":
+        # the fused kernel also runs the length-64 DFTs over n2: 5 n log2 n
+        # flops per complex transform, K*C forward and K*ceil(C/2) inverse
+        # columns per class
+        n1 = N // 64
+        dft = 5 * 64 * 6
+        flops += dft * B * n1 * K * (C + Cp)
+        flop_model += f" + {dft}-flop length-64 DFTs on {B * n1 * K * (C + Cp)} columns"
+    achieved_tflops = flops / (cg_ms * 1e-3) / 1e12
+    counters, traffic_src = committed_counters(args.workload) if not args.bf16 else (None, "bf16 run")
+    traffic = counters["cg_hbm_bytes_per_launch"] if counters else None
     roofline = {
-        "kernel": f"cg_gen_kernel<{L}>",
+        "kernel": f"{'cg_fused_kernel' if dom == 'cg_fused' else 'cg_gen_kernel'}<{L}>",
         "bound": "alu",
         "achieved": round(achieved_tflops, 2),
         "peak": round(VALU_PEAK_TFLOPS, 1),
@@ -222,9 +241,8 @@ def main():
         "frac": round(achieved_tflops / VALU_PEAK_TFLOPS, 4),
         "traffic": traffic,
         "traffic_source": traffic_src,
-        "flops_per_launch": points * cg_flops_per_point,
-        "flop_model": f"(6*{n_products} distinct complex products + 4*{nnz} non-zeros) per "
-                      f"(b, frequency 0..N/2, channel) point, {points} points",
+        "flops_per_launch": flops,
+        "flop_model": flop_model,
         "launch_ms": round(cg_ms, 4),
         "frac_of_packed_fp32_peak": round(achieved_tflops / VALU_PEAK_PACKED_TFLOPS, 4),
     }
@@ -245,7 +263,11 @@ def main():
         "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C,
                    "parallelism": "single GPU"},
         "hbm": {"algorithmic_bytes_per_step": 3 * S, "achieved_gbs": round(hbm_alg_gbs, 1),
-                "peak_gbs": HBM_PEAK_GBS, "frac": round(hbm_alg_gbs / HBM_PEAK_GBS, 4)},
+                "peak_gbs": HBM_PEAK_GBS, "frac": round(hbm_alg_gbs / HBM_PEAK_GBS, 4),
+                "counter_bytes_per_step": counters["step_hbm_bytes"] if counters else None,
+                "counter_gbs": round(counters["step_hbm_bytes"] / (ms * 1e-3) / 1e9, 1) if counters else None,
+                "counter_frac": round(counters["step_hbm_bytes"] / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4)
+                if counters else None},
         "roofline": roofline,
         "stages": stages,
     }
