@@ -247,3 +247,50 @@ def test_argument_errors_on_gpu():
         assert "allocation" in P.cgconv_last_error()
     finally:
         del os.environ["CGCONV_TEST_FAIL_ALLOC"]
+
+
+# Shapes on the fused pipeline (512 <= N <= 16384, L <= 6): C = 1, L = 0,
+# channel counts that leave a ragged last block of 4, both ends of the N
+# range.  The fused result must agree with the modular pipeline and with
+# the oracle.
+FUSED_SHAPES = [(2, 512, 4, 1), (1, 16384, 0, 3), (3, 1024, 6, 4), (1, 2048, 5, 7), (2, 4096, 3, 2),
+                (1, 8192, 1, 5)]
+
+
+@pytest.mark.parametrize("shape", FUSED_SHAPES, ids=lambda s: "B%dN%dL%dC%d" % s)
+def test_fused_matches_modular_and_oracle(shape):
+    B, N, L, C = shape
+    q, k = W.iid(B, N, L, C, seed=9100 + N + L + C)
+    a = gpu_forward(q, k, L, tag="fused " + str(shape))
+    b = gpu_forward(q, k, L, env={"CGCONV_UNFUSED": "1"}, tag="modular " + str(shape))
+    assert rel_l2(a, b) <= 1e-5
+    ref = cgconv_fft(q, k, L)
+    err = rel_l2(a, ref)
+    print(f"  fused {shape}: rel_l2 = {err:.3e}", flush=True)
+    assert err <= TOL_F32
+
+
+def test_fused_bf16():
+    q, k = W.iid(2, 2048, 6, 8, seed=77)
+    qb, kb = W.to_bf16_bits(q), W.to_bf16_bits(k)
+    got = gpu_forward(qb, kb, 6, bf16=True, tag="fused bf16")
+    ref = cgconv_fft(W.bf16_bits_to_f32(qb), W.bf16_bits_to_f32(kb), 6)
+    assert rel_l2(got, ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("N,L,expect", [(256, 3, ["fft_fwd", "cg", "fft_inv"]),
+                                        (1024, 3, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
+                                        (16384, 6, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
+                                        (32768, 2, ["fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"]),
+                                        (1024, 7, ["fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"])])
+def test_plan_picks_pipeline(N, L, expect):
+    torch = _torch()
+    import paper_2509_24093_amd as P
+    print(f"[gpu] pipeline choice N={N} L={L}", flush=True)
+    plan = P.Plan(1, N, L, 2)
+    q = torch.zeros(plan.shape, device="cuda")
+    plan.enable_timing(1)
+    plan(q, q)
+    times, calls = plan.stage_times()
+    assert calls == 1 and list(times) == expect
+    plan.close()
