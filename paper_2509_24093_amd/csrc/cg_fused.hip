@@ -58,14 +58,13 @@ __device__ __forceinline__ float2 conjf2(float2 v) { return make_float2(v.x, -v.
 template <int L>
 struct FusedStore {
   static constexpr int PMAX = Geo<L>::PMAX;
-  float2* slot;    // LDS: this lane's slot ci = 0 in O1; slot ci at slot[2 * ci]
-  float2* O1;      // LDS: packed outputs of the current phase [cls][w2][ci][pair]
-  float2* O2;      // LDS: scratch of the inverse transform (aliases the forward tile)
-  const float2* tw64;   // LDS: exp(-2 pi i x / 64)
+  float2* slot;         // LDS: this lane's slot ci = 0 in O1; slot ci at slot[2 * ci]
+  float2* O1;           // LDS: packed outputs of the current phase [cls][w2][ci][pair]
+  float2* O2;           // LDS: scratch of the inverse transform (aliases the forward tile)
+  const float2* tw8;    // LDS: [t][j] exp(-2 pi i j t / 64), j, t < 8
   const float2* twp;    // LDS: [cls][n2] exp(+2 pi i n2 w1_cls / N)
-  float2* V;
-  float2* vtrash;       // global: target of masked V stores
-  long long rowbase0, rowbase1;  // first V row of each class, batch included
+  const char* Vb;       // V of this batch element (bytes)
+  unsigned rowoff0, rowoff1;  // first V row of each class within the batch element
   int tid, cb, Cp;
   bool even, selfpaired;
 
@@ -81,44 +80,52 @@ struct FusedStore {
     slot[2 * ci] = even ? make_float2(u.x - v.y, u.y + v.x) : make_float2(v.x + u.y, u.x - v.y);
   }
 
+  // Inverse length-64 DFT over w2 of the phase's columns (cls, ci, pair):
+  // radix 8 from O1 into O2, then radix 8 with the twiddles W_64^(-j2 t),
+  // the inter-pass twiddle and the store of V rows.  Item it = (column, j);
+  // the LDS and V addresses of an item are a per-item base plus constants.
   __device__ __forceinline__ void end_phase(int mu) const {
+    constexpr int K = Geo<L>::K;
     const int nc = mu == 0 ? L + 1 : 2 * (L + 1 - mu);
     const int ncol = 2 * nc * 2;  // (cls, ci, pair)
     __syncthreads();              // every lane has parked its outputs
     for (int it = tid; it < ncol * 8; it += kThreadsF) {
       const int col = it % ncol, j1 = it / ncol;
       const int pair = col & 1, ci = (col >> 1) % nc, cls = (col >> 1) / nc;
+      const float2* src = O1 + ((cls * kN2 + j1) * PMAX + ci) * 2 + pair;
+      float2* dst = O2 + ((cls * kN2 + j1 * 8) * PMAX + ci) * 2 + pair;
       float2 x[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) x[t] = O1[((cls * kN2 + j1 + 8 * t) * PMAX + ci) * 2 + pair];
+      for (int t = 0; t < 8; ++t) x[t] = src[8 * t * PMAX * 2];
       dft_reg<8, 1>(x);
 #pragma unroll
-      for (int s = 0; s < 8; ++s) O2[((cls * kN2 + j1 * 8 + s) * PMAX + ci) * 2 + pair] = x[s];
+      for (int s = 0; s < 8; ++s) dst[s * PMAX * 2] = x[s];
     }
     __syncthreads();
     for (int it = tid; it < ncol * 8; it += kThreadsF) {
       const int col = it % ncol, j2 = it / ncol;
       const int pair = col & 1, ci = (col >> 1) % nc, cls = (col >> 1) / nc;
+      const float2* src = O2 + ((cls * kN2 + j2) * PMAX + ci) * 2 + pair;
+      const float2* tw = tw8 + j2;
       float2 x[8];
+      x[0] = src[0];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        x[t] = O2[((cls * kN2 + j2 + 8 * t) * PMAX + ci) * 2 + pair];
-        if (t > 0 && j2 > 0) x[t] = cmul(x[t], conjf2(tw64[j2 * t]));
-      }
+      for (int t = 1; t < 8; ++t) x[t] = cmul(src[8 * t * PMAX * 2], conjf2(tw[8 * t]));
       dft_reg<8, 1>(x);
       const int J = mu == 0 ? ci : mu + (ci >> 1);
       const int M = mu == 0 ? 0 : ((ci & 1) ? -mu : mu);
       const int kout = J * J + J + M;
       const int gp = 2 * cb + pair;
-      const bool ok = gp < Cp && !(selfpaired && cls == 1);
-      const long long rb = cls ? rowbase1 : rowbase0;
-      const int K = (L + 1) * (L + 1);
+      if (gp < Cp && !(selfpaired && cls == 1)) {
+        const float2* tp = twp + cls * kN2 + j2;
+        const unsigned off = (((cls ? rowoff1 : rowoff0) + (unsigned)j2) * (unsigned)K + (unsigned)kout) *
+                                 (unsigned)Cp * 8u + (unsigned)gp * 8u;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int n2 = j2 + 8 * s;
-        const float2 val = cmul(x[s], twp[cls * kN2 + n2]);
-        float2* dst = ok ? &V[((rb + n2) * K + kout) * Cp + gp] : &vtrash[tid];
-        *dst = val;
+        for (int s = 0; s < 8; ++s) {
+          // rows n2 = j2 + 8 s: a uniform byte offset per s
+          const char* vs = Vb + (size_t)(8 * s) * K * Cp * 8;
+          *reinterpret_cast<float2*>(const_cast<char*>(vs) + off) = cmul(x[s], tp[8 * s]);
+        }
       }
     }
   }
@@ -133,8 +140,8 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
   // the forward they become the output tiles: O1 is the tile the last chunk
   // did not use, O2 the one it did.
   __shared__ float2 sT[2][G::T_ELEMS];
-  __shared__ float2 sTw[kN2];
-  __shared__ float2 sTwp[2 * kN2];
+  __shared__ float2 sTw8[kN2];       // [t][j] exp(-2 pi i j t / 64)
+  __shared__ float2 sTwp[2 * kN2];   // [cls][n2] exp(+2 pi i n2 w1_cls / N)
 
   // XCD-aware block order: the Cb channel blocks of one class pair have
   // block ids equal mod 8 (same XCD, same L2) and are dispatched together.
@@ -148,14 +155,15 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
   const long long N = a.N;
   const int w1b = (N1 - w1) & (N1 - 1);
   const bool selfpaired = w1b == w1;
-  const long long row0 = (long long)b * N + (long long)w1 * kN2;
-  const long long row1 = (long long)b * N + (long long)w1b * kN2;
   const int tid = threadIdx.x;
   const int p = tid >> 2, cc = tid & 3;
   const int pp = w1 == 0 ? ((kN2 - p) & (kN2 - 1)) : (kN2 - 1 - p);
   const int C = a.C;
 
-  for (int x = tid; x < kN2; x += kThreadsF) sTw[x] = a.tw[(long long)x * (N / kN2)];
+  for (int x = tid; x < kN2; x += kThreadsF) {
+    const int t = x >> 3, j = x & 7;
+    sTw8[x] = a.tw[(long long)(j * t) * (N / kN2)];
+  }
   for (int x = tid; x < 2 * kN2; x += kThreadsF) {
     const int cls = x / kN2, n2 = x % kN2;
     const long long e = ((long long)n2 * (cls ? w1b : w1)) & (N - 1);
@@ -166,72 +174,89 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
   constexpr int NCOL = 2 * KC * kCc;  // columns (cls, kk, cc) of one chunk
   constexpr int NITEM = NCOL * 8;     // stage items (column, j)
   static_assert(NITEM <= 2 * kThreadsF, "at most two stage items per thread");
-  // Stage-1 inputs of a chunk: item it = (column, j1) needs rows
-  // n2 = j1 + 8t of its column.  Every address is valid (item indices
-  // beyond NITEM and padding channels alias a real element); the values are
-  // zeroed where they must not contribute.
-  auto load_item = [&](int q, int it, float2 (&x)[8]) {
-    const bool live = it < NITEM;
-    const int itc = live ? it : 0;
-    const int col = itc % NCOL, j1 = itc / NCOL;
+  // Item it = (column, j) of a chunk: stage 1 transforms rows j + 8t of its
+  // column, stage 2 the rows 8j' + j after the exchange.  Its addresses do
+  // not depend on the chunk: Y byte offset within the batch element (the
+  // chunk and t add uniform offsets), and the LDS bases of both stages.
+  // Items past NITEM alias item 0 for the loads and store nothing; padding
+  // channels (C not a multiple of 4) read channel C-1, whose spectrum is
+  // again that of a real signal, so the channel-pair packing stays exact
+  // for the real channel it is paired with and nothing needs zeroing.
+  struct Item {
+    unsigned goff;  // byte offset of row j of the column, chunk 0
+    int lds1, lds2;
+    bool live;
+  };
+  auto make_item = [&](int it) {
+    Item m;
+    m.live = it < NITEM;
+    const int itc = m.live ? it : 0;
+    const int col = itc % NCOL, j = itc / NCOL;
     const int icc = col % kCc, kk = (col / kCc) % KC, cls = col / (kCc * KC);
     const int ch = 4 * cb + icc;
     const int chl = ch < C ? ch : C - 1;
-    const bool use = live && ch < C;
-    const long long rb = cls ? row1 : row0;
+    m.goff = ((unsigned)((cls ? w1b : w1) * kN2 + j) * (unsigned)K + (unsigned)kk) * (unsigned)C * 8u +
+             (unsigned)chl * 8u;
+    m.lds1 = ((cls * kN2 + j * 8) * KC + kk) * kCc + icc;
+    m.lds2 = ((cls * kN2 + j) * KC + kk) * kCc + icc;
+    return m;
+  };
+  const Item it0 = make_item(tid), it1 = make_item(tid + kThreadsF);
+  const char* const Yb = reinterpret_cast<const char*>(a.Y + (long long)b * N * K * C);
+  auto load_item = [&](int q, const Item& m, float2 (&x)[8]) {
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-      const float2 v = a.Y[((rb + j1 + 8 * t) * K + q * KC + kk) * C + chl];
-      x[t] = use ? v : make_float2(0.f, 0.f);
+      const char* sb = Yb + ((long long)(8 * t) * K * C + (long long)q * KC * C) * 8;  // uniform
+      x[t] = *reinterpret_cast<const float2*>(sb + m.goff);
     }
   };
-  auto stage1_store = [&](float2* sTO, int it, float2 (&x)[8]) {
-    if (it < NITEM) {
-      const int col = it % NCOL, j1 = it / NCOL;
-      const int icc = col % kCc, kk = (col / kCc) % KC, cls = col / (kCc * KC);
+  auto stage1_store = [&](float2* sTO, const Item& m, float2 (&x)[8]) {
+    if (m.live) {
       dft_reg<8, -1>(x);
+      float2* d = sTO + m.lds1;
 #pragma unroll
-      for (int s2 = 0; s2 < 8; ++s2) sTO[((cls * kN2 + j1 * 8 + s2) * KC + kk) * kCc + icc] = x[s2];
+      for (int s2 = 0; s2 < 8; ++s2) d[s2 * KC * kCc] = x[s2];
     }
   };
+  auto stage2 = [&](float2* sTO, const Item& m, int j2) {
+    float2* d = sTO + m.lds2;
+    const float2* tw = sTw8 + j2;
+    float2 x[8];
+    x[0] = d[0];
+#pragma unroll
+    for (int t = 1; t < 8; ++t) x[t] = cmul(d[8 * t * KC * kCc], tw[8 * t]);
+    dft_reg<8, -1>(x);
+#pragma unroll
+    for (int s2 = 0; s2 < 8; ++s2) d[8 * s2 * KC * kCc] = x[s2];
+  };
+  const int j2_0 = tid / NCOL, j2_1 = (tid + kThreadsF) / NCOL;
   // All chunks' HBM loads are issued up front (as many loads in flight as
   // the unfused kernel has): every chunk consumed frees 32 raw registers and
   // fills 28 input registers, so the peak is the raw data itself.
   float2 raw[L + 1][2][8];
 #pragma unroll
   for (int q = 0; q < L + 1; ++q) {
-    load_item(q, tid, raw[q][0]);
-    load_item(q, tid + kThreadsF, raw[q][1]);
+    load_item(q, it0, raw[q][0]);
+    load_item(q, it1, raw[q][1]);
   }
 #pragma unroll
   for (int q = 0; q < L + 1; ++q) {
-    float2(&c0)[8] = raw[q][0];
-    float2(&c1)[8] = raw[q][1];
     float2* sTO = sT[q & 1];
     // stage 1: radix 8 over n2 = j1 + 8t (inputs already in registers)
-    stage1_store(sTO, tid, c0);
-    stage1_store(sTO, tid + kThreadsF, c1);
+    stage1_store(sTO, it0, raw[q][0]);
+    stage1_store(sTO, it1, raw[q][1]);
     __syncthreads();
     // stage 2: twiddle W_64^(j2 t), radix 8; reads and writes rows j2 + 8t
-    for (int it = tid; it < NITEM; it += kThreadsF) {
-      const int col = it % NCOL, j2 = it / NCOL;
-      const int icc = col % kCc, kk = (col / kCc) % KC, cls = col / (kCc * KC);
-      float2 x[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        x[t] = sTO[((cls * kN2 + j2 + 8 * t) * KC + kk) * kCc + icc];
-        if (t > 0 && j2 > 0) x[t] = cmul(x[t], sTw[j2 * t]);
-      }
-      dft_reg<8, -1>(x);
-#pragma unroll
-      for (int s2 = 0; s2 < 8; ++s2) sTO[((cls * kN2 + j2 + 8 * s2) * KC + kk) * kCc + icc] = x[s2];
-    }
+    if (it0.live) stage2(sTO, it0, j2_0);
+    if (it1.live) stage2(sTO, it1, j2_1);
     __syncthreads();
     // gather this lane's frequency pair: Z_w (class 0, p), Z_{N-w} (class 1, pp)
+    const float2* g0 = sTO + (0 * kN2 + p) * KC * kCc + cc;
+    const float2* g1 = sTO + (1 * kN2 + pp) * KC * kCc + cc;
 #pragma unroll
     for (int kk = 0; kk < KC; ++kk) {
-      const float2 A = sTO[((0 * kN2 + p) * KC + kk) * kCc + cc];
-      const float2 B = sTO[((1 * kN2 + pp) * KC + kk) * kCc + cc];
+      const float2 A = g0[kk * kCc];
+      const float2 B = g1[kk * kCc];
       qa[q * KC + kk] = make_float2(A.x + B.x, A.y - B.y);  // 2Q
       ka[q * KC + kk] = make_float2(A.y + B.y, B.x - A.x);  // 2K
     }
@@ -250,12 +275,11 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
                           : &sO1[(1 * kN2 + pp) * G::PMAX * 2 + (cc >> 1)];
   st.O1 = sO1;
   st.O2 = sT[L & 1];
-  st.tw64 = sTw;
+  st.tw8 = sTw8;
   st.twp = sTwp;
-  st.V = a.V;
-  st.vtrash = a.vtrash;
-  st.rowbase0 = row0;
-  st.rowbase1 = row1;
+  st.Vb = reinterpret_cast<const char*>(a.V + (long long)b * N * K * a.Cp);
+  st.rowoff0 = (unsigned)(w1 * kN2);
+  st.rowoff1 = (unsigned)(w1b * kN2);
   st.tid = tid;
   st.cb = cb;
   st.Cp = a.Cp;
@@ -269,6 +293,8 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
 template <>
 hipError_t launch_cg_fused<CGCONV_TU_L>(const FusedArgs& a, hipStream_t s) {
   if (a.N1 < 2 || a.N != (long long)a.N1 * kN2 || a.Cb != (a.C + kCc - 1) / kCc) return hipErrorInvalidValue;
+  // per-batch-element byte offsets of Y are 32-bit
+  if ((long double)a.N * Geo<CGCONV_TU_L>::K * a.C * 8 >= 4294967296.0L) return hipErrorInvalidValue;
   const long long units = (long long)a.B * a.units;
   const long long blocks = 8LL * a.Cb * ((units + 7) / 8);
   hipLaunchKernelGGL(cg_fused_kernel<CGCONV_TU_L>, dim3((unsigned)blocks), dim3(kThreadsF), 0, s, a);

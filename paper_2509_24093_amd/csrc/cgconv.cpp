@@ -198,7 +198,6 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     FusedArgs fa;
     fa.Y = p->ws1;
     fa.V = p->ws2;
-    fa.vtrash = p->ws2 + p->B * N * K * p->Cp;
     fa.tw = p->tw;
     fa.N = N;
     fa.N1 = N1;
@@ -330,7 +329,10 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
   p->K = K;
   if (const char* env = std::getenv("CGCONV_FORCE_GENERIC")) p->force_generic = env[0] == '1';
   const char* unfused = std::getenv("CGCONV_UNFUSED");
-  if (N >= 512 && N <= 16384 && L_max <= kFusedLmax && !(unfused && unfused[0] == '1') && !p->force_generic) {
+  // the fused kernel addresses one batch element's spectra with 32-bit byte offsets
+  const bool fits32 = (long double)N * K * C * 8 < 4294967296.0L;
+  if (N >= 512 && N <= 16384 && L_max <= kFusedLmax && fits32 && !(unfused && unfused[0] == '1') &&
+      !p->force_generic) {
     p->fused = true;
     p->N2 = 64;
     p->N1 = N / 64;

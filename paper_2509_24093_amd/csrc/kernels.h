@@ -90,7 +90,6 @@ hipError_t launch_cg_gen(const CgArgs& a, hipStream_t s);
 struct FusedArgs {
   const float2* Y;
   float2* V;
-  float2* vtrash;    // >= 256 float2: target of masked stores
   const float2* tw;  // exp(-2 pi i j / N)
   long long N;
   int N1;            // N / 64
