@@ -131,3 +131,51 @@ def test_wrong_racah_prefactor_is_caught(monkeypatch):
         return np.sign(s) * sqrt(pre * s * s)
     monkeypatch.setattr(ocg, "cg_complex", bad)
     assert not _orthogonal()
+
+
+def _mix_pins_hold():
+    """The mixed oracle's degree-map pins (output degree and query degree)."""
+    from oracle.cg import paths
+    from oracle.mix import cgconv_mixed_direct
+    rng = np.random.default_rng(41)
+    L, N, C = 2, 5, 3
+    q, k = rng.normal(size=(1, N, 9, C)), rng.normal(size=(1, N, 9, C))
+    A = [rng.normal(size=(C, C)) for _ in range(L + 1)]
+    W = np.stack([A[J] for (_, _, J) in paths(L)])
+    got = cgconv_mixed_direct(q, k, L, W)
+    u = oconv.cgconv_direct(q, k, L)
+    ok = all(np.abs(got[:, :, J * J:(J + 1) ** 2] - np.einsum("dc,bnmc->bnmd", A[J], u[:, :, J * J:(J + 1) ** 2])).max() < 1e-10
+             for J in range(L + 1))
+    s = rng.normal(size=L + 1)
+    W = np.stack([s[l1] * np.eye(C) for (l1, _, _) in paths(L)])
+    qs = q * np.repeat(s, [2 * l + 1 for l in range(L + 1)])[None, None, :, None]
+    return ok and np.abs(cgconv_mixed_direct(q, k, L, W) - oconv.cgconv_direct(qs, k, L)).max() < 1e-10
+
+
+def test_mix_pins_hold_unmutated():
+    assert _mix_pins_hold()
+
+
+@pytest.mark.parametrize("plant", ["transpose_W", "swap_l1_l2", "wrong_degree_slot"])
+def test_mixing_mistakes_are_caught(monkeypatch, plant):
+    import oracle.mix as omix
+    orig_paths = omix.paths
+    orig_mix = omix._mix_products
+    if plant == "transpose_W":
+        monkeypatch.setattr(omix, "_mix_products", lambda P, L, W: orig_mix(P, L, np.swapaxes(W, 1, 2)))
+    elif plant == "swap_l1_l2":
+        # weights attached to (l2, l1, J) instead of (l1, l2, J)
+        def bad(P, L, W):
+            idx = {p: n for n, p in enumerate(orig_paths(L))}
+            Wp = np.stack([W[idx[(l2, l1, J)]] for (l1, l2, J) in orig_paths(L)])
+            return orig_mix(P, L, Wp)
+        monkeypatch.setattr(omix, "_mix_products", bad)
+    else:
+        # output of path (l1, l2, J) added at the slot of degree J - 1 when J > 0
+        def bad(P, L, W):
+            out = orig_mix(P, L, W)
+            if L >= 2:
+                out[..., 1:4, :], out[..., 4:9, :][..., :3, :] = out[..., 4:9, :][..., :3, :].copy(), out[..., 1:4, :].copy()
+            return out
+        monkeypatch.setattr(omix, "_mix_products", bad)
+    assert not _mix_pins_hold()
