@@ -59,7 +59,9 @@ enum cgconv_status {
  * batch >= 1; N >= 2 and a power of two, N <= CGCONV_NMAX; 0 <= L_max <=
  * CGCONV_LMAX; C >= 1.  Builds the sparse CG table (§4.3) and the FFT
  * twiddles on the host, allocates the device workspace (hipMalloc on the
- * current device, 2 * batch*N*(L_max+1)^2*C*8 bytes) and uploads the tables.
+ * current device, 2 * batch*N*(L_max+1)^2*C*8 bytes, plus 4 KiB per path for
+ * the channel-mixing weights when L_max <= 6 and C <= 32) and uploads the
+ * tables.
  * Synchronous.  Returns NULL on failure (see cgconv_last_error()).
  */
 cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_t C);
@@ -81,6 +83,35 @@ int cgconv_forward(cgconv_plan_t plan, const float* q, const float* k, float* ou
  */
 int cgconv_forward_bf16(cgconv_plan_t plan, const uint16_t* q, const uint16_t* k,
                         uint16_t* out, hipStream_t stream);
+
+/*
+ * CG convolution with per-path channel mixing (the inter-channel form of
+ * §4.1: the depthwise product of every path is mixed over channels by one
+ * dense weight matrix per path before the paths are summed):
+ *
+ *   out[b,i,(J,M),c] = sum_{p=(l1,l2,J)} sum_{c'} W_p[c,c']
+ *                      * sum_{m1,m2} R^{(l1 l2 J)}[M,m1,m2]
+ *                      * sum_j q[b,j,(l1,m1),c'] * k[b,(i-j) mod N,(l2,m2),c']
+ *
+ * weights: DEVICE pointer, fp32 [n_paths][C][C] (row = output channel c,
+ * column = input channel c'), 16-byte aligned, paths in the order of
+ * cgconv_paths.  W_p = identity for every p gives cgconv_forward.  q, k, out
+ * as for cgconv_forward (fp32).  The dense mixing runs on the matrix cores
+ * (fp32 MFMA); the unfused FFT passes are used.  Needs L_max <= 6 and C <= 32
+ * (CGCONV_ERR_UNSUPPORTED otherwise).  Same stream and workspace rules as
+ * cgconv_forward; the weights are read during the call only.
+ */
+int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, const float* weights,
+                         float* out, hipStream_t stream);
+
+/*
+ * Host-only (no GPU needed): the CG paths at L_max in the order the mixing
+ * weights use, every triangle-allowed (l1, l2, J) with l1, l2, J <= L_max
+ * (odd l1+l2+J included), lexicographic in (l1, l2, J).  Writes up to cap
+ * triples to l1l2J[3*p .. 3*p+2] (may be NULL when cap == 0) and returns the
+ * number of paths, or a negative status.
+ */
+int64_t cgconv_paths(int32_t L_max, int32_t* l1l2J, int64_t cap);
 
 /* Free the plan's device workspace and tables.  NULL is a no-op. */
 void cgconv_plan_destroy(cgconv_plan_t plan);
@@ -125,8 +156,11 @@ int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, 
  * summed time of each stage in milliseconds to ms[0 .. min(cap, n_stages)-1];
  * n_stages and n_calls (may be NULL) receive the stage count (3 for N <= 256:
  * fft_fwd, cg, fft_inv; 5 above: fft_fwd_1, fft_fwd_2, cg, fft_inv_1,
- * fft_inv_2) and the number of timed calls.  cgconv_plan_stage_name returns
- * a stage's name ("" if out of range).
+ * fft_inv_2; for plans with 512 <= N <= 16384 and L_max <= 6: fft_fwd_1,
+ * cg_fused, fft_inv_2) and the number of timed calls.  The first timed call
+ * fixes whether plain or mixed forwards are timed (mixed: cg_mix replaces cg
+ * and the unfused passes are listed); calls of the other kind are not timed.
+ * cgconv_plan_stage_name returns a stage's name ("" if out of range).
  */
 int cgconv_plan_enable_timing(cgconv_plan_t plan, int32_t max_calls);
 int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t* n_stages, int32_t* n_calls);

@@ -52,6 +52,10 @@ def library() -> ctypes.CDLL:
     lib.cgconv_forward.restype = ctypes.c_int
     lib.cgconv_forward_bf16.argtypes = [vp, vp, vp, vp, vp]
     lib.cgconv_forward_bf16.restype = ctypes.c_int
+    lib.cgconv_forward_mixed.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.cgconv_forward_mixed.restype = ctypes.c_int
+    lib.cgconv_paths.argtypes = [i32, ctypes.POINTER(i32), i64]
+    lib.cgconv_paths.restype = i64
     lib.cgconv_plan_destroy.argtypes = [vp]
     lib.cgconv_plan_destroy.restype = None
     lib.cgconv_plan_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64),
@@ -101,6 +105,23 @@ def cgconv_forward(plan: int, q: int, k: int, out: int, stream: int) -> int:
 
 def cgconv_forward_bf16(plan: int, q: int, k: int, out: int, stream: int) -> int:
     return _check(library().cgconv_forward_bf16(plan, q, k, out, stream))
+
+
+def cgconv_forward_mixed(plan: int, q: int, k: int, weights: int, out: int, stream: int) -> int:
+    """Per-path channel mixing; weights: device fp32 [n_paths][C][C]."""
+    return _check(library().cgconv_forward_mixed(plan, q, k, weights, out, stream))
+
+
+def cgconv_paths(L_max: int):
+    """The CG paths (l1, l2, J) in the order of the mixing weights (host only);
+    returns an int32 (n_paths, 3) array."""
+    import numpy as np
+    lib = library()
+    n = _check(lib.cgconv_paths(L_max, None, 0))
+    out = np.zeros((n, 3), dtype=np.int32)
+    got = _check(lib.cgconv_paths(L_max, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n))
+    assert got == n
+    return out
 
 
 def cgconv_plan_destroy(plan: int) -> None:
@@ -197,6 +218,21 @@ class Plan:
             cgconv_forward_bf16(self._h, q.data_ptr(), k.data_ptr(), out.data_ptr(), s)
         else:
             raise ValueError("q, k must be float32 or bfloat16")
+        return out
+
+    def forward_mixed(self, q, k, weights, out=None):
+        """Per-path channel mixing (fp32): weights [n_paths, C, C], paths in
+        the order of :func:`cgconv_paths`."""
+        import torch
+        if out is None:
+            out = torch.empty(self.shape, dtype=torch.float32, device=q.device)
+        s = self._args(q, k, out, torch.float32)
+        P = self.info()[0]
+        C = self.shape[3]
+        if (not isinstance(weights, torch.Tensor) or not weights.is_cuda or weights.dtype != torch.float32
+                or tuple(weights.shape) != (P, C, C) or not weights.is_contiguous()):
+            raise ValueError(f"weights must be a contiguous float32 GPU tensor of shape {(P, C, C)}")
+        cgconv_forward_mixed(self._h, q.data_ptr(), k.data_ptr(), weights.data_ptr(), out.data_ptr(), s)
         return out
 
     __call__ = forward

@@ -89,7 +89,23 @@ __global__ __launch_bounds__(kGenThreads) void cg_generic_kernel(CgArgs a) {
   }
 }
 
+__global__ void prepare_mix_weights_kernel(const float* __restrict__ W, float* __restrict__ wt, int paths, int C) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;  // (path, step, lane)
+  if (i >= (long long)paths * 16 * 64) return;
+  const int lane = (int)(i % 64), step = (int)((i / 64) % 16);
+  const long long p = i / (16 * 64);
+  const int co = lane % 32, ci = 2 * step + lane / 32;
+  wt[i] = (co < C && ci < C) ? W[(p * C + co) * C + ci] : 0.f;
+}
+
 }  // namespace
+
+hipError_t launch_prepare_mix_weights(const float* W, float* wt, int paths, int C, hipStream_t s) {
+  if (!W || !wt || paths <= 0 || C <= 0 || C > kMixCmax) return hipErrorInvalidValue;
+  const long long n = (long long)paths * 16 * 64;
+  hipLaunchKernelGGL(prepare_mix_weights_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, W, wt, paths, C);
+  return hipGetLastError();
+}
 
 int cg_generated_lmax() { return CGCONV_LGEN; }
 

@@ -11,6 +11,8 @@ namespace cgdev {
 
 template <int L>
 struct CgBody;  // specialised by the generated cg_body_L<L>.inc files
+template <int L>
+struct CgPathBody;  // per-path variant for the channel-mixing kernel (same files)
 
 constexpr int kCgThreads = 256;
 

@@ -68,11 +68,13 @@ struct cgconv_plan {
   int* d_offs = nullptr;
   uint32_t* d_tkey = nullptr;
   float* d_tcoef = nullptr;
+  float* d_wmix = nullptr;  // channel-mixing weights in MFMA operand order (L <= 6, C <= 32)
   bool force_generic = false;
-  // optional per-stage timing: events recorded on the forward's stream
-  int n_stages = 0;
-  int timing_max = 0, timing_calls = 0;
-  std::vector<hipEvent_t> events;  // timing_max * (n_stages + 1)
+  // optional per-stage timing: events recorded on the forward's stream.  The
+  // first timed call fixes the kind (plain or mixed) that is timed.
+  int n_stages = 0, n_stages_mix = 0;
+  int timing_max = 0, timing_calls = 0, timing_kind = -1;
+  std::vector<hipEvent_t> events;  // timing_max * kMaxEvents
 };
 
 namespace {
@@ -88,6 +90,7 @@ void free_plan(cgconv_plan* p) {
   (void)hipFree(p->d_offs);
   (void)hipFree(p->d_tkey);
   (void)hipFree(p->d_tcoef);
+  (void)hipFree(p->d_wmix);
   for (hipEvent_t ev : p->events) (void)hipEventDestroy(ev);
   (void)hipSetDevice(cur);
   delete p;
@@ -96,6 +99,22 @@ void free_plan(cgconv_plan* p) {
 const char* const kStages2[] = {"fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"};
 const char* const kStages1[] = {"fft_fwd", "cg", "fft_inv"};
 const char* const kStagesF[] = {"fft_fwd_1", "cg_fused", "fft_inv_2"};
+const char* const kStagesM2[] = {"fft_fwd_1", "fft_fwd_2", "cg_mix", "fft_inv_1", "fft_inv_2"};
+const char* const kStagesM1[] = {"fft_fwd", "cg_mix", "fft_inv"};
+constexpr int kMaxEvents = 6;  // stages + 1 of the longest pipeline
+
+hipError_t launch_mix(int L, const CgArgs& a, hipStream_t s) {
+  switch (L) {
+    case 0: return launch_cg_mix<0>(a, s);
+    case 1: return launch_cg_mix<1>(a, s);
+    case 2: return launch_cg_mix<2>(a, s);
+    case 3: return launch_cg_mix<3>(a, s);
+    case 4: return launch_cg_mix<4>(a, s);
+    case 5: return launch_cg_mix<5>(a, s);
+    case 6: return launch_cg_mix<6>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_fused(int L, const FusedArgs& a, hipStream_t s) {
   switch (L) {
@@ -131,7 +150,10 @@ PassArgs base_args(const cgconv_plan* p) {
   return a;
 }
 
-int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf16, hipStream_t s) {
+// weights != nullptr: the channel-mixing stage with the unfused passes
+int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf16, hipStream_t s,
+                const float* weights = nullptr) {
+  const bool mix = weights != nullptr;
   const int K = p->K;
   const long long Wz = (long long)K * p->C;   // complex columns of z
   const long long Ww = (long long)K * p->Cp;  // complex columns of the packed output spectra
@@ -174,13 +196,16 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
   ca.offs = p->d_offs;
   ca.tkey = p->d_tkey;
   ca.tcoef = p->d_tcoef;
+  ca.wmix = p->d_wmix;
   ca.n1_log2 = ilog2(p->N1 ? p->N1 : p->N);
   ca.n2_log2 = ilog2(p->N1 ? p->N2 : 1);
   const long long N = p->N;
   const float inv_n = 1.0f / (float)N;
   hipEvent_t* ev = nullptr;  // events of this call if it is timed
-  if (p->timing_calls < p->timing_max) {
-    ev = &p->events[(size_t)p->timing_calls * (p->n_stages + 1)];
+  const int kind = mix ? 1 : 0;
+  if (p->timing_calls < p->timing_max && (p->timing_kind < 0 || p->timing_kind == kind)) {
+    p->timing_kind = kind;
+    ev = &p->events[(size_t)p->timing_calls * kMaxEvents];
     ++p->timing_calls;
   }
   int stage = 0;
@@ -189,7 +214,11 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     ++stage;
   };
   mark();
-  if (p->fused) {
+  if (mix) {
+    e = launch_prepare_mix_weights(weights, p->d_wmix, (int)p->paths, (int)p->C, s);
+    if (e != hipSuccess) goto fail;
+  }
+  if (p->fused && !mix) {
     // F1 (Y rows w1*64 + n2) -> fused F2 + CG + I1 (V rows w1*64 + n2) -> I2
     const int N1 = (int)p->N1, N2 = 64;
     e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
@@ -220,7 +249,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     ca.Z = p->ws1;
     ca.W = p->ws2;
     ca.trash = p->ws2 + p->B * N * K * p->Cp;
-    e = launch_cg(p->L, ca, p->force_generic, s);
+    e = mix ? launch_mix(p->L, ca, s) : launch_cg(p->L, ca, p->force_generic, s);
     if (e != hipSuccess) goto fail;
     mark();
     e = pass((int)N, IN_COMPLEX, out_split, 1, 1, p->ws2, nullptr, out, N * Ww, N * K * p->C, (int)Ww, 0, 1, 0, 1,
@@ -240,7 +269,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     ca.Z = p->ws2;
     ca.W = p->ws1;
     ca.trash = p->ws1 + p->B * N * K * p->Cp;
-    e = launch_cg(p->L, ca, p->force_generic, s);
+    e = mix ? launch_mix(p->L, ca, s) : launch_cg(p->L, ca, p->force_generic, s);
     if (e != hipSuccess) goto fail;
     mark();
     e = pass(N2, IN_COMPLEX, OUT_COMPLEX, 1, N1, p->ws1, nullptr, p->ws2, N * Ww, N * Ww, (int)Ww, N2, 1, N2, 1, 1,
@@ -342,6 +371,7 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
     p->N2 = N / p->N1;
   }
   p->n_stages = (p->N1 && !p->fused) ? 5 : 3;
+  p->n_stages_mix = p->N1 ? 5 : 3;
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) {
     set_error("hipGetDevice failed: %s", hipGetErrorString(e));
@@ -401,6 +431,16 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
     free_plan(p);
     return nullptr;
   }
+  if (L_max <= kMixLmax && C <= kMixCmax) {
+    // prepared channel-mixing weights, [paths][16][64] floats
+    if ((e = hipMalloc(&p->d_wmix, (size_t)p->paths * 16 * 64 * sizeof(float))) != hipSuccess) {
+      set_error("mixing-weight allocation failed: %s", hipGetErrorString(e));
+      (void)hipGetLastError();
+      free_plan(p);
+      return nullptr;
+    }
+    p->ws_bytes += (size_t)p->paths * 16 * 64 * sizeof(float);
+  }
   return p;
 }
 
@@ -428,7 +468,8 @@ int cgconv_plan_enable_timing(cgconv_plan_t plan, int32_t max_calls) {
   plan->events.clear();
   plan->timing_max = 0;
   plan->timing_calls = 0;
-  const size_t n = (size_t)max_calls * (plan->n_stages + 1);
+  plan->timing_kind = -1;
+  const size_t n = (size_t)max_calls * kMaxEvents;
   plan->events.reserve(n);
   for (size_t i = 0; i < n; ++i) {
     hipEvent_t ev;
@@ -450,12 +491,12 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
     set_error("plan is NULL or ms is NULL");
     return CGCONV_ERR_INVALID_ARG;
   }
-  const int ns = plan->n_stages;
+  const int ns = plan->timing_kind == 1 ? plan->n_stages_mix : plan->n_stages;
   if (n_stages) *n_stages = ns;
   if (n_calls) *n_calls = plan->timing_calls;
   for (int st = 0; st < cap && st < ns; ++st) ms[st] = 0.0;
   for (int c = 0; c < plan->timing_calls; ++c) {
-    hipEvent_t* ev = &plan->events[(size_t)c * (ns + 1)];
+    hipEvent_t* ev = &plan->events[(size_t)c * kMaxEvents];
     hipError_t e = hipEventSynchronize(ev[ns]);
     if (e != hipSuccess) {
       set_error("hipEventSynchronize failed: %s", hipGetErrorString(e));
@@ -475,7 +516,12 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
 }
 
 const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
-  if (!plan || stage < 0 || stage >= plan->n_stages) return "";
+  if (!plan || stage < 0) return "";
+  if (plan->timing_kind == 1) {
+    if (stage >= plan->n_stages_mix) return "";
+    return plan->N1 ? kStagesM2[stage] : kStagesM1[stage];
+  }
+  if (stage >= plan->n_stages) return "";
   if (plan->fused) return kStagesF[stage];
   return plan->N1 ? kStages2[stage] : kStages1[stage];
 }
@@ -491,6 +537,49 @@ int cgconv_forward_bf16(cgconv_plan_t plan, const uint16_t* q, const uint16_t* k
   const int st = check_forward_args(plan, q, k, out);
   if (st != CGCONV_OK) return st;
   return run_forward(plan, q, k, out, true, stream);
+}
+
+int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, const float* weights, float* out,
+                         hipStream_t stream) {
+  const int st = check_forward_args(plan, q, k, out);
+  if (st != CGCONV_OK) return st;
+  if (!weights) {
+    set_error("weights must be a non-NULL device pointer");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!aligned16(weights)) {
+    set_error("weights must be 16-byte aligned");
+    return CGCONV_ERR_ALIGNMENT;
+  }
+  if (!plan->d_wmix) {
+    set_error("channel mixing needs L_max <= %d and C <= %d (plan: L_max=%d, C=%lld)", kMixLmax, kMixCmax, plan->L,
+              (long long)plan->C);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  return run_forward(plan, q, k, out, false, stream, weights);
+}
+
+int64_t cgconv_paths(int32_t L_max, int32_t* l1l2J, int64_t cap) {
+  if (L_max < 0 || L_max > CGCONV_LMAX) {
+    set_error("unsupported L_max=%d", L_max);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  if (cap < 0 || (cap > 0 && !l1l2J)) {
+    set_error("invalid output buffer");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  int64_t n = 0;
+  for (int l1 = 0; l1 <= L_max; ++l1)
+    for (int l2 = 0; l2 <= L_max; ++l2)
+      for (int J = std::abs(l1 - l2); J <= std::min(l1 + l2, (int)L_max); ++J) {
+        if (n < cap) {
+          l1l2J[3 * n] = l1;
+          l1l2J[3 * n + 1] = l2;
+          l1l2J[3 * n + 2] = J;
+        }
+        ++n;
+      }
+  return n;
 }
 
 int64_t cgconv_cg_table(int32_t L_max, int32_t* idx, double* coef, int64_t cap) {

@@ -32,6 +32,9 @@
 // cg_common.h): written as ordinary C++, the compiler turns -(a*b) into
 // a*(-b) and keeps a negated copy of every input alive for the whole kernel.
 //
+// A second body per L, CgPathBody<L>, keeps the paths apart for the
+// channel-mixing kernel (see emit_path_body).
+//
 // Usage: gen_cg <output-dir> <LGEN>   (writes cg_body_L<L>.inc and cg_lgen.h)
 #include <algorithm>
 #include <array>
@@ -320,6 +323,88 @@ void emit_body(FILE* f, int L, long* ops_out) {
 
 }  // namespace
 
+// Per-path body for the channel-mixing kernel (CgPathBody<L>::run): the
+// products of every path p = (l1, l2, J) are kept apart.  Pairs (l1, l2) are
+// taken in lexicographic order, so path indices follow the same (l1, l2, J)
+// order as the weights.  Inside a pair the outputs are produced by M, with
+// the products qa[l1,m1] * ka[l2,M-m1] (4 ops) shared by all J of the pair;
+// every value w_p[M] goes to st.put(slot, value) with slot = the position of
+// (J, M) among the pair's outputs (J ascending, then M = -J..J), zeros
+// included, and st.end_pair<p0, Jmin, Jmax>() follows the pair's last value.
+void emit_path_body(FILE* f, int L, long* ops_out) {
+  const int K = (L + 1) * (L + 1);
+  std::vector<Term> terms = contraction_terms(L);
+  std::map<std::array<int, 4>, std::vector<Term>> by_pair_M;  // (l1, l2, M, -) -> terms
+  for (const Term& t : terms) by_pair_M[{t.l1, t.l2, t.M, 0}].push_back(t);
+  long ops = 0;
+  int path = 0, max_slots = 0;
+  std::fprintf(f, "template <>\nstruct CgPathBody<%d> {\n  static constexpr int K = %d;\n", L, K);
+  std::fprintf(f, "  template <class Store>\n");
+  std::fprintf(f,
+               "  static __device__ __forceinline__ void run(const float2 (&qa)[%d], const float2 (&ka)[%d], "
+               "Store& st) {\n",
+               K, K);
+  for (int l1 = 0; l1 <= L; ++l1)
+    for (int l2 = 0; l2 <= L; ++l2) {
+      const int Jmin = std::abs(l1 - l2), Jmax = std::min(l1 + l2, L);
+      if (Jmin > Jmax) continue;
+      int slots = 0;
+      for (int J = Jmin; J <= Jmax; ++J) slots += 2 * J + 1;
+      max_slots = std::max(max_slots, slots);
+      std::fprintf(f, "    {  // pair l1=%d l2=%d: paths %d..%d (J = %d..%d)\n", l1, l2, path, path + Jmax - Jmin,
+                   Jmin, Jmax);
+      for (int M = -Jmax; M <= Jmax; ++M) {
+        auto it = by_pair_M.find({l1, l2, M, 0});
+        std::map<int, std::vector<const Term*>> by_m1;
+        if (it != by_pair_M.end())
+          for (const Term& t : it->second) by_m1[t.m1].push_back(&t);
+        std::fprintf(f, "    {  // M = %d\n", M);
+        std::set<int> inited;
+        for (int J = std::max(Jmin, std::abs(M)); J <= Jmax; ++J) std::fprintf(f, "      float2 t%d;\n", J);
+        for (auto& e : by_m1) {
+          const int m1 = e.first, m2 = M - m1;
+          const std::string q = qname(l1, m1), k = kname(l2, m2);
+          std::fprintf(f, "      { const float pr = fnma(%s.y, %s.y, %s.x * %s.x);", q.c_str(), k.c_str(), q.c_str(),
+                       k.c_str());
+          std::fprintf(f, " const float pi = fmaf(%s.y, %s.x, %s.x * %s.y);\n", q.c_str(), k.c_str(), q.c_str(),
+                       k.c_str());
+          ops += 4;
+          for (const Term* t : e.second) {
+            const std::string a = "t" + std::to_string(t->J);
+            const std::string re_src = t->imag ? "pi" : "pr", im_src = t->imag ? "pr" : "pi";
+            const double re_c = t->imag ? -t->coef : t->coef, im_c = t->coef;
+            if (!inited.count(t->J))
+              std::fprintf(f, "      %s.x = %s * %s; %s.y = %s * %s;\n", a.c_str(), lit(re_c).c_str(),
+                           re_src.c_str(), a.c_str(), lit(im_c).c_str(), im_src.c_str());
+            else
+              std::fprintf(f, "      %s.x = fmaf(%s, %s, %s.x); %s.y = fmaf(%s, %s, %s.y);\n", a.c_str(),
+                           lit(re_c).c_str(), re_src.c_str(), a.c_str(), a.c_str(), lit(im_c).c_str(),
+                           im_src.c_str(), a.c_str());
+            inited.insert(t->J);
+            ops += 2;
+          }
+          std::fprintf(f, "      }\n");
+        }
+        int base = 0;
+        for (int J = Jmin; J <= Jmax; ++J) {
+          if (std::abs(M) <= J) {
+            if (!inited.count(J)) std::fprintf(f, "      t%d = make_float2(0.f, 0.f);\n", J);
+            std::fprintf(f, "      st.put(%d, t%d);\n", base + M + J, J);
+          }
+          base += 2 * J + 1;
+        }
+        std::fprintf(f, "    }\n");
+      }
+      std::fprintf(f, "      st.template end_pair<%d, %d, %d>();\n    }\n", path, Jmin, Jmax);
+      path += Jmax - Jmin + 1;
+    }
+  std::fprintf(f, "  }\n");
+  std::fprintf(f, "  static constexpr int kPaths = %d;\n", path);
+  std::fprintf(f, "  static constexpr int kMaxPairSlots = %d;  // most outputs (J, M) of one pair\n", max_slots);
+  std::fprintf(f, "  static constexpr long kOps = %ld;  // VALU ops of the per-path products per point\n};\n\n", ops);
+  *ops_out = ops;
+}
+
 int main(int argc, char** argv) {
   if (argc != 3) {
     std::fprintf(stderr, "usage: %s <output-dir> <LGEN>\n", argv[0]);
@@ -336,10 +421,11 @@ int main(int argc, char** argv) {
     }
     std::fprintf(f, "// Generated by csrc/codegen/gen_cg.cpp -- do not edit.\n");
     std::fprintf(f, "// Frequency-domain CG contraction body, L_max = %d.\n#pragma once\n\n", L);
-    long ops = 0;
+    long ops = 0, pops = 0;
     emit_body(f, L, &ops);
+    emit_path_body(f, L, &pops);
     std::fclose(f);
-    std::fprintf(stderr, "gen_cg: L=%d ops/point=%ld\n", L, ops);
+    std::fprintf(stderr, "gen_cg: L=%d ops/point=%ld per-path ops/point=%ld\n", L, ops, pops);
   }
   const std::string hpath = dir + "/cg_lgen.h";
   FILE* h = std::fopen(hpath.c_str(), "w");

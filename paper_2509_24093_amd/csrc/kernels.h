@@ -74,6 +74,9 @@ struct CgArgs {
   const int* offs;       // [K+1] term offsets per complex-basis output index
   const uint32_t* tkey;  // k1 | k2 << 8 | imag << 16
   const float* tcoef;
+  // channel-mixing kernel only: weights in the MFMA A-operand order,
+  // [path][16 steps][64 lanes], lane l of step s = W_p[l % 32][2 s + l / 32]
+  const float* wmix;
 };
 
 hipError_t launch_cg(int L, const CgArgs& a, bool force_generic, hipStream_t s);
@@ -82,6 +85,17 @@ hipError_t launch_cg(int L, const CgArgs& a, bool force_generic, hipStream_t s);
 // the translation unit built for that L).
 template <int L>
 hipError_t launch_cg_gen(const CgArgs& a, hipStream_t s);
+
+// Channel-mixing CG stage (cg_mix.hip), one specialisation per L_max <= 6:
+// same Z / W layouts as the unmixed stage, C <= 32.
+template <int L>
+hipError_t launch_cg_mix(const CgArgs& a, hipStream_t s);
+constexpr int kMixLmax = 6;
+constexpr int kMixCmax = 32;
+
+// W: [paths][C][C] fp32 (row = output channel) -> wt in the A-operand order
+// above, zero outside C x C.
+hipError_t launch_prepare_mix_weights(const float* W, float* wt, int paths, int C, hipStream_t s);
 
 // Fused second forward pass + CG stage + first inverse pass for two-pass
 // plans with N2 = 64 (see cg_fused.hip).  Y: output of the first forward

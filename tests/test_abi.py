@@ -106,3 +106,21 @@ def test_timing_entry_points_reject_null_plan():
     assert lib.cgconv_plan_enable_timing(None, 4) == P.CGCONV_ERR_INVALID_ARG
     assert lib.cgconv_plan_stage_times(None, None, 0, None, None) == P.CGCONV_ERR_INVALID_ARG
     assert lib.cgconv_plan_stage_name(None, 0) == b""
+
+
+@pytest.mark.parametrize("L", range(0, 9))
+def test_paths_match_oracle_order(L):
+    """The weight order of the mixing entry point is the oracle's path list."""
+    from oracle.cg import paths
+    got = [tuple(int(x) for x in row) for row in P.cgconv_paths(L)]
+    assert got == paths(L)
+
+
+def test_mixed_entry_points_reject_bad_arguments():
+    lib = P.library()
+    assert lib.cgconv_forward_mixed(None, 16, 16, 16, 32, None) == P.CGCONV_ERR_INVALID_ARG
+    assert lib.cgconv_paths(9, None, 0) == P.CGCONV_ERR_UNSUPPORTED
+    assert lib.cgconv_paths(2, None, 3) == P.CGCONV_ERR_INVALID_ARG
+    buf = (ctypes.c_int32 * 6)(*([-7] * 6))
+    n = lib.cgconv_paths(2, buf, 2)
+    assert n == 15 and buf[5] != -7
