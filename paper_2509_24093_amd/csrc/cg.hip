@@ -90,10 +90,12 @@ __global__ __launch_bounds__(kGenThreads) void cg_generic_kernel(CgArgs a) {
 }
 
 __global__ void prepare_mix_weights_kernel(const float* __restrict__ W, float* __restrict__ wt, int paths, int C) {
-  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;  // (path, step, lane)
+  // wt[((p * 4 + s / 4) * 64 + lane) * 4 + s % 4] = W_p[lane % 32][2 s + lane / 32]
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (long long)paths * 16 * 64) return;
-  const int lane = (int)(i % 64), step = (int)((i / 64) % 16);
-  const long long p = i / (16 * 64);
+  const int s_lo = (int)(i % 4), lane = (int)((i / 4) % 64), s_hi = (int)((i / 256) % 4);
+  const long long p = i / 1024;
+  const int step = 4 * s_hi + s_lo;
   const int co = lane % 32, ci = 2 * step + lane / 32;
   wt[i] = (co < C && ci < C) ? W[(p * C + co) * C + ci] : 0.f;
 }

@@ -19,7 +19,9 @@
 // every lane reads back its 49 mixed complex-basis values, converts them to
 // the real basis and stores them channel-pair packed, exactly like the
 // unmixed stage.  Weights arrive pre-arranged in the MFMA A-operand order
-// (prepare_mix_weights).
+// (prepare_mix_weights) and are copied per pair straight into LDS
+// (global_load_lds), overlapping the pair's VALU products; both MFMA
+// operands are then read as 16-byte LDS loads, 4 steps at a time.
 #include <hip/hip_runtime.h>
 
 #include "cg_common.h"
@@ -46,47 +48,79 @@ struct MixGeo {
   static constexpr int NTW = (NT + kWaves - 1) / kWaves;  // tiles per wave
   static constexpr int NOUT = 32 * NT;                    // output columns (tile g at 32 g)
   static constexpr int NIN = 16 * CgPathBody<L>::kMaxPairSlots + 16;  // staging of one pair (+ overrun of a half tile)
-  static constexpr int COLS = NOUT > NIN ? NOUT : NIN;
-  static constexpr int STRIDE = (COLS + 63) / 64 * 64 + 2;  // row stride = 2 mod 64 words: rows on distinct banks
-  static_assert(32 * STRIDE * 4 <= 160 * 1024, "LDS staging exceeds 160 KB");
+  // A column holds its 32 channels in the order c' = 2 s + k -> 16 k + s,
+  // so that MFMA step s reads element 16 k + s; rows of 36 words keep the
+  // 16-byte reads of 16 consecutive lanes on distinct banks.
+  static constexpr int RS = 36;
+  static constexpr int NPAIR = L + 1;                      // most paths of one (l1, l2) pair
+  static constexpr int T_WORDS = NIN * RS;
+  static constexpr int W_WORDS = NPAIR * 1024;             // weights of one pair, MFMA A order
+  static constexpr int P_WORDS = NOUT * RS;                // parked output tiles
+  static constexpr int WORDS = (T_WORDS + W_WORDS) > P_WORDS ? (T_WORDS + W_WORDS) : P_WORDS;
+  static_assert(WORDS * 4 <= 160 * 1024, "LDS exceeds 160 KB");
 };
+
+__device__ __forceinline__ int perm32(int c) { return 16 * (c & 1) + (c >> 1); }
 
 template <int L>
 struct MixStore {
   using G = MixGeo<L>;
-  float* stage;      // LDS [32 c][STRIDE]
-  const float* wt;   // prepared weights: [path][16 steps][64 lanes]
-  int lane, wave, c, pt;
+  float* stage;      // LDS: staged values [col][RS] (channel order perm32)
+  float* wst;        // LDS: weights of the current pair [path][4][64][4]
+  const float* wt;   // prepared weights (global), same order per path
+  int lane, wave, pc, pt;  // pc = perm32(channel)
   v16f acc[G::NTW];
 
-  // value of slot s of the current pair (s = position of (J, M) among the
-  // pair's outputs): columns 16 s + 2 pt + {0, 1}
+  // weights of the pair's paths P0 .. P0+NP-1 into LDS (1 KB per wave
+  // instruction, straight from global memory); they arrive while the
+  // pair's products are computed
+  template <int P0, int NP>
+  __device__ __forceinline__ void begin_pair() {
+#pragma unroll
+    for (int ch = wave; ch < 4 * NP; ch += kWaves) {
+      const float* src = wt + ((long long)P0 * 4 + ch) * 256 + lane * 4;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(wst + ch * 256), 16, 0, 0);
+    }
+  }
+
+  // value of slot s of the current pair: columns 16 s + 2 pt + {0, 1}
   __device__ __forceinline__ void put(int slot, float2 v) {
-    *reinterpret_cast<float2*>(stage + c * G::STRIDE + slot * 16 + pt * 2) = v;
+    float* d = stage + (slot * 16 + pt * 2) * G::RS + pc;
+    d[0] = v.x;
+    d[G::RS] = v.y;
   }
 
   template <int P0, int JMIN, int JMAX>
   __device__ __forceinline__ void end_pair() {
-    __syncthreads();  // the pair's values are staged
-    int colJ = 0;     // first staging column of degree J within the pair
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's weight copies have landed
+    __syncthreads();                // every value and weight is staged
+    int colJ = 0;                   // first staging column of degree J within the pair
 #pragma unroll
     for (int J = JMIN; J <= JMAX; ++J) {
-      const int p = P0 + J - JMIN;
 #pragma unroll
       for (int t = 0; t <= J; ++t) {
         const int g = J * (J + 1) / 2 + t;  // global output tile
         if (wave == g % kWaves) {
+          const float4* wa = reinterpret_cast<const float4*>(wst + (J - JMIN) * 1024 + lane * 4);
+          const float4* tb = reinterpret_cast<const float4*>(stage + (colJ + 32 * t + (lane & 31)) * G::RS +
+                                                             16 * (lane >> 5));
           v16f d = acc[g / kWaves];
-          const float* wp = wt + (long long)p * 16 * 64 + lane;
-          const float* bp = stage + (lane >> 5) * G::STRIDE + colJ + 32 * t + (lane & 31);
 #pragma unroll
-          for (int s = 0; s < 16; ++s) d = __builtin_amdgcn_mfma_f32_32x32x2f32(wp[s * 64], bp[2 * s * G::STRIDE], d, 0, 0, 0);
+          for (int s4 = 0; s4 < 4; ++s4) {
+            const float4 a = wa[s4 * 64];
+            const float4 b = tb[s4];
+            d = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, b.x, d, 0, 0, 0);
+            d = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, b.y, d, 0, 0, 0);
+            d = __builtin_amdgcn_mfma_f32_32x32x2f32(a.z, b.z, d, 0, 0, 0);
+            d = __builtin_amdgcn_mfma_f32_32x32x2f32(a.w, b.w, d, 0, 0, 0);
+          }
           acc[g / kWaves] = d;
         }
       }
       colJ += 16 * (2 * J + 1);
     }
-    __syncthreads();  // before the next pair overwrites the staging
+    __syncthreads();  // before the next pair overwrites values and weights
   }
 };
 
@@ -94,10 +128,10 @@ template <int L>
 __global__ __launch_bounds__(kMixThreads, 1) void cg_mix_kernel(CgArgs a) {
   using G = MixGeo<L>;
   constexpr int K = G::K;
-  __shared__ float stage[32 * G::STRIDE];
+  __shared__ __attribute__((aligned(16))) float smem[G::WORDS];
   const int tid = threadIdx.x;
   const long long gp = (long long)blockIdx.x * kMixPts + tid / kMixCh;
-  const long long npts = (a.npts / (2 * a.Cp)) ;  // B * F points
+  const long long npts = a.npts / (2 * a.Cp);  // B * F points
   Point pt;
   pt.valid = gp < npts;
   const long long gpc = pt.valid ? gp : 0;
@@ -108,41 +142,45 @@ __global__ __launch_bounds__(kMixThreads, 1) void cg_mix_kernel(CgArgs a) {
   load_unpack<K>(a, pt, qa, ka);
 
   MixStore<L> st;
-  st.stage = stage;
+  st.stage = smem;
+  st.wst = smem + G::T_WORDS;
   st.wt = a.wmix;
   st.lane = tid & 63;
   st.wave = tid >> 6;
-  st.c = pt.c;
+  st.pc = perm32(pt.c);
   st.pt = tid / kMixCh;
 #pragma unroll
   for (int i = 0; i < G::NTW; ++i) st.acc[i] = v16f{};
   CgPathBody<L>::run(qa, ka, st);
 
-  // park the mixed tiles: D row i = c_out, column 32 g + (lane & 31)
+  // park the mixed tiles: D row i = c_out, column 32 g + (lane & 31), stored
+  // as [column][RS] with the channels in natural order
 #pragma unroll
   for (int g = 0; g < G::NT; ++g) {
     if (st.wave == g % kWaves) {
+      float* col = smem + (32 * g + (st.lane & 31)) * G::RS + 4 * (st.lane >> 5);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = 8 * (r / 4) + 4 * (st.lane >> 5) + (r % 4);
-        stage[i * G::STRIDE + 32 * g + (st.lane & 31)] = st.acc[g / kWaves][r];
-      }
+      for (int r = 0; r < 16; ++r) col[8 * (r / 4) + (r % 4)] = st.acc[g / kWaves][r];
     }
   }
   __syncthreads();
-  // this lane's mixed complex-basis values w[J, M]: column 32 J(J+1)/2 + 16 (M+J) + 2 pt
+  // this lane's mixed complex-basis values w[J, M] (columns 32 J(J+1)/2 +
+  // 16 (M+J) + 2 pt + {0, 1}), converted to the real basis and stored
+  // channel-pair packed as in the unmixed stage
   Point ps = pt;
   ps.valid = pt.valid && pt.c < 2 * a.Cp;
   PairStore out = make_store(a, ps, K);
-  const float* row = stage + pt.c * G::STRIDE + 2 * st.pt;
+  const float* base = smem + (2 * st.pt) * G::RS + pt.c;
+  auto w_at = [&](int J, int M) {
+    const float* e = base + (32 * (J * (J + 1) / 2) + 16 * (M + J)) * G::RS;
+    return make_float2(e[0], e[G::RS]);
+  };
 #pragma unroll
   for (int J = 0; J <= L; ++J) {
-    const float* rj = row + 32 * (J * (J + 1) / 2) + 16 * J;  // M = 0
-    out(J * J + J, *reinterpret_cast<const float2*>(rj));
+    out(J * J + J, w_at(J, 0));
 #pragma unroll
     for (int mu = 1; mu <= J; ++mu) {
-      const float2 wp = *reinterpret_cast<const float2*>(rj + 16 * mu);
-      const float2 wm = *reinterpret_cast<const float2*>(rj - 16 * mu);
+      const float2 wp = w_at(J, mu), wm = w_at(J, -mu);
       out(J * J + J + mu, make_float2(wm.x + wp.x, wm.y + wp.y));  // U[J,+mu] = w[J,-mu] + w[J,+mu]
       out(J * J + J - mu, make_float2(wm.y - wp.y, wp.x - wm.x));  // U[J,-mu] = i (w[J,+mu] - w[J,-mu])
     }

@@ -330,7 +330,8 @@ void emit_body(FILE* f, int L, long* ops_out) {
 // the products qa[l1,m1] * ka[l2,M-m1] (4 ops) shared by all J of the pair;
 // every value w_p[M] goes to st.put(slot, value) with slot = the position of
 // (J, M) among the pair's outputs (J ascending, then M = -J..J), zeros
-// included, and st.end_pair<p0, Jmin, Jmax>() follows the pair's last value.
+// included; st.begin_pair<p0, n_paths>() precedes the pair's first value and
+// st.end_pair<p0, Jmin, Jmax>() follows its last one.
 void emit_path_body(FILE* f, int L, long* ops_out) {
   const int K = (L + 1) * (L + 1);
   std::vector<Term> terms = contraction_terms(L);
@@ -353,6 +354,7 @@ void emit_path_body(FILE* f, int L, long* ops_out) {
       max_slots = std::max(max_slots, slots);
       std::fprintf(f, "    {  // pair l1=%d l2=%d: paths %d..%d (J = %d..%d)\n", l1, l2, path, path + Jmax - Jmin,
                    Jmin, Jmax);
+      std::fprintf(f, "      st.template begin_pair<%d, %d>();\n", path, Jmax - Jmin + 1);
       for (int M = -Jmax; M <= Jmax; ++M) {
         auto it = by_pair_M.find({l1, l2, M, 0});
         std::map<int, std::vector<const Term*>> by_m1;

@@ -75,7 +75,8 @@ struct CgArgs {
   const uint32_t* tkey;  // k1 | k2 << 8 | imag << 16
   const float* tcoef;
   // channel-mixing kernel only: weights in the MFMA A-operand order,
-  // [path][16 steps][64 lanes], lane l of step s = W_p[l % 32][2 s + l / 32]
+  // [path][4][64 lanes][4]: element (p, s / 4, l, s % 4) = W_p[l % 32][2 s + l / 32]
+  // for step s = 0..15, so that one 1 KB block holds 4 steps of every lane
   const float* wmix;
 };
 
