@@ -89,22 +89,30 @@ __global__ __launch_bounds__(kGenThreads) void cg_generic_kernel(CgArgs a) {
   }
 }
 
-__global__ void prepare_mix_weights_kernel(const float* __restrict__ W, float* __restrict__ wt, int paths, int C) {
-  // wt[((p * 4 + s / 4) * 64 + lane) * 4 + s % 4] = W_p[lane % 32][2 s + lane / 32]
+// bfloat16 bits of x, round to nearest even (inputs are finite)
+__device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__global__ void prepare_mix_weights_kernel(const float* __restrict__ W, uint16_t* __restrict__ wt, int paths,
+                                           int C) {
+  // element (p, s, h, lane, e) at ((((p * 2 + s) * 2 + h) * 64 + lane) * 8 + e)
   const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (long long)paths * 16 * 64) return;
-  const int s_lo = (int)(i % 4), lane = (int)((i / 4) % 64), s_hi = (int)((i / 256) % 4);
-  const long long p = i / 1024;
-  const int step = 4 * s_hi + s_lo;
-  const int co = lane % 32, ci = 2 * step + lane / 32;
-  wt[i] = (co < C && ci < C) ? W[(p * C + co) * C + ci] : 0.f;
+  if (i >= (long long)paths * 2048) return;
+  const int e = (int)(i % 8), lane = (int)((i / 8) % 64), h = (int)((i / 512) % 2), step = (int)((i / 1024) % 2);
+  const long long p = i / 2048;
+  const int co = lane % 32, ci = 16 * step + 8 * (lane / 32) + e;
+  const float w = (co < C && ci < C) ? W[(p * C + co) * C + ci] : 0.f;
+  const uint32_t hi = bf16_bits_rne(w);
+  wt[i] = (uint16_t)(h == 0 ? hi : bf16_bits_rne(w - __uint_as_float(hi << 16)));
 }
 
 }  // namespace
 
-hipError_t launch_prepare_mix_weights(const float* W, float* wt, int paths, int C, hipStream_t s) {
+hipError_t launch_prepare_mix_weights(const float* W, uint16_t* wt, int paths, int C, hipStream_t s) {
   if (!W || !wt || paths <= 0 || C <= 0 || C > kMixCmax) return hipErrorInvalidValue;
-  const long long n = (long long)paths * 16 * 64;
+  const long long n = (long long)paths * 2048;
   hipLaunchKernelGGL(prepare_mix_weights_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, W, wt, paths, C);
   return hipGetLastError();
 }

@@ -68,7 +68,7 @@ struct cgconv_plan {
   int* d_offs = nullptr;
   uint32_t* d_tkey = nullptr;
   float* d_tcoef = nullptr;
-  float* d_wmix = nullptr;  // channel-mixing weights in MFMA operand order (L <= 6, C <= 32)
+  uint16_t* d_wmix = nullptr;  // channel-mixing weights, split bf16 MFMA operands (L <= 6, C <= 32)
   bool force_generic = false;
   // optional per-stage timing: events recorded on the forward's stream.  The
   // first timed call fixes the kind (plain or mixed) that is timed.
@@ -432,14 +432,14 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
     return nullptr;
   }
   if (L_max <= kMixLmax && C <= kMixCmax) {
-    // prepared channel-mixing weights, [paths][16][64] floats
-    if ((e = hipMalloc(&p->d_wmix, (size_t)p->paths * 16 * 64 * sizeof(float))) != hipSuccess) {
+    // prepared channel-mixing weights, 2048 bf16 per path
+    if ((e = hipMalloc(&p->d_wmix, (size_t)p->paths * 2048 * sizeof(uint16_t))) != hipSuccess) {
       set_error("mixing-weight allocation failed: %s", hipGetErrorString(e));
       (void)hipGetLastError();
       free_plan(p);
       return nullptr;
     }
-    p->ws_bytes += (size_t)p->paths * 16 * 64 * sizeof(float);
+    p->ws_bytes += (size_t)p->paths * 2048 * sizeof(uint16_t);
   }
   return p;
 }

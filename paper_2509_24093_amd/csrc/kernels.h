@@ -74,10 +74,11 @@ struct CgArgs {
   const int* offs;       // [K+1] term offsets per complex-basis output index
   const uint32_t* tkey;  // k1 | k2 << 8 | imag << 16
   const float* tcoef;
-  // channel-mixing kernel only: weights in the MFMA A-operand order,
-  // [path][4][64 lanes][4]: element (p, s / 4, l, s % 4) = W_p[l % 32][2 s + l / 32]
-  // for step s = 0..15, so that one 1 KB block holds 4 steps of every lane
-  const float* wmix;
+  // channel-mixing kernel only: weights split into bfloat16 hi + lo parts
+  // (W = hi + lo + O(2^-18 W)) in the A-operand order of
+  // v_mfma_f32_32x32x16_bf16, [path][step s (2)][hi/lo][lane (64)][8]:
+  // lane l of step s holds W_p[l % 32][16 s + 8 (l / 32) + e], e = 0..7
+  const uint16_t* wmix;
 };
 
 hipError_t launch_cg(int L, const CgArgs& a, bool force_generic, hipStream_t s);
@@ -94,9 +95,9 @@ hipError_t launch_cg_mix(const CgArgs& a, hipStream_t s);
 constexpr int kMixLmax = 6;
 constexpr int kMixCmax = 32;
 
-// W: [paths][C][C] fp32 (row = output channel) -> wt in the A-operand order
-// above, zero outside C x C.
-hipError_t launch_prepare_mix_weights(const float* W, float* wt, int paths, int C, hipStream_t s);
+// W: [paths][C][C] fp32 (row = output channel) -> wt in the split A-operand
+// order above (4 KiB per path), zero outside C x C.
+hipError_t launch_prepare_mix_weights(const float* W, uint16_t* wt, int paths, int C, hipStream_t s);
 
 // Fused second forward pass + CG stage + first inverse pass for two-pass
 // plans with N2 = 64 (see cg_fused.hip).  Y: output of the first forward
