@@ -20,7 +20,10 @@ Prints ONE JSON line.  Besides the contract fields it carries
 Flags: --gpus N (only 1 is supported), --steps K, --warmup W,
 --no-cpu-baseline, --cpu-seconds S, --workload NAME (other synthetic
 workloads, for exploration), --bf16, --copy-calibration (a plain device copy
-of known size, the reference for rocprofv3 byte counters).
+of known size, the reference for rocprofv3 byte counters), --mixed (the
+convolution with per-path channel mixing, cgconv_forward_mixed, with seeded
+random weights: its own JSON line, the mixing stage against the bf16 matrix
+core peak).
 """
 
 from __future__ import annotations
@@ -42,6 +45,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 VALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 VALU_PEAK_PACKED_TFLOPS = 157.3
 METRIC = "CG-conv tokens/sec at N=16384, L_max=6, C=32; achieved HBM GB/s vs peak"
+METRIC_MIXED = "CG-conv with per-path channel mixing, tokens/sec at N=16384, L_max=6, C=32"
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
 CG_SOURCES = ["paper_2509_24093_amd/csrc/cg_gen.hip", "paper_2509_24093_amd/csrc/cg_fused.hip",
               "paper_2509_24093_amd/csrc/cg_common.h", "paper_2509_24093_amd/csrc/fft_reg.h",
               "paper_2509_24093_amd/csrc/codegen/gen_cg.cpp", "paper_2509_24093_amd/csrc/cg_table.cpp",
@@ -146,6 +151,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--mixed", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: this build runs on one GPU only "
@@ -181,6 +187,9 @@ def main():
         esize = 4
     out = torch.empty_like(qd)
     plan = P.Plan(B, N, L, C)
+    if args.mixed:
+        bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C)
+        return
     n_paths, nnz, n_products, ws_bytes = plan.info()
     log(f"[bench] plan: paths={n_paths} nnz={nnz} products={n_products} workspace={ws_bytes / 2**30:.2f} GiB")
 
@@ -281,6 +290,97 @@ def main():
         result["cpu_baseline"] = obj
         result["parity_rel_l2_sampled_rows"] = parity
         log(f"[bench] parity on {R} rows: rel_l2 = {parity:.3e}")
+    else:
+        result["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(result), flush=True)
+
+
+def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
+    """cgconv_forward_mixed on the same inputs with weights W_p ~ N(0, 1/C)."""
+    import numpy as np
+    import torch
+
+    import paper_2509_24093_amd as P
+    paths = [tuple(int(x) for x in row) for row in P.cgconv_paths(L)]
+    n_paths = len(paths)
+    wts = (np.random.default_rng(2025).normal(size=(n_paths, C, C)) / np.sqrt(C)).astype(np.float32)
+    wd = torch.from_numpy(wts).cuda()
+    for _ in range(args.warmup):
+        plan.forward_mixed(qd, kd, wd, out)
+    torch.cuda.synchronize()
+    plan.enable_timing(args.steps)
+    log(f"[bench] timing {args.steps} mixed steps")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        plan.forward_mixed(qd, kd, wd, out)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    stage_ms, ncalls = plan.stage_times()
+    stage_avg = {s: v / max(ncalls, 1) for s, v in stage_ms.items()}
+    mix_ms = stage_avg["cg_mix"]
+    F = N // 2 + 1
+    pts = B * F
+    outs = int(sum(2 * J + 1 for _, _, J in paths))          # per-path outputs (J, M) per channel
+    mix_flops = 4 * outs * C * C * pts                        # real W x complex T, multiply-add
+    pair_tiles = sum(J + 1 for _, _, J in paths)               # tile passes per 8 points
+    mfma_flops = 6 * 32 * 32 * 16 * 2 * pair_tiles * ((pts + 7) // 8)  # bf16 MFMAs executed
+    achieved = mfma_flops / (mix_ms * 1e-3) / 1e12
+    result = {
+        "metric": METRIC_MIXED,
+        "value": B * N / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 (mixing: bf16 hi/lo split on MFMA, fp32 accumulate)",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C, "paths": n_paths,
+                   "weights": "N(0, 1/C), seed 2025", "parallelism": "single GPU"},
+        "roofline": {
+            "kernel": f"cg_mix_kernel<{L}>",
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+            "flops_per_launch": mfma_flops,
+            "flop_model": (f"bf16 MFMA flops executed: 6 v_mfma_f32_32x32x16_bf16 (3 per 16 input channels, "
+                           f"hi/lo split) per 32x32 tile pass, {pair_tiles} tile passes per 8 points, "
+                           f"{(pts + 7) // 8} blocks of 8 points; the fp32-equivalent mixing work is "
+                           f"4*{outs}*C^2 per point = {mix_flops} flops"),
+            "mixing_tflops_fp32_equivalent": round(mix_flops / (mix_ms * 1e-3) / 1e12, 2),
+            "launch_ms": round(mix_ms, 4),
+        },
+        "stages": {s: {"ms": round(t, 4)} for s, t in stage_avg.items()},
+    }
+    if not args.no_cpu_baseline:
+        from oracle.mix import cgconv_mixed_direct_rows
+        log(f"[bench] CPU oracle baseline, mixed (~{args.cpu_seconds:.0f} s)")
+        got = out.cpu().numpy()
+        rng = np.random.default_rng(2026)
+        rows, ref = [], []
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_seconds or len(rows) < 2:
+            part = [(int(rng.integers(0, B)), int(rng.integers(0, N)))]
+            if not rows:
+                part = [(0, 0)]
+            ref.extend(cgconv_mixed_direct_rows(q, k, L, wts, part))
+            rows.extend(part)
+        dt = time.perf_counter() - t0
+        num = sum(float(((got[b, i].astype(np.float64) - ref[n]) ** 2).sum()) for n, (b, i) in enumerate(rows))
+        den = sum(float((r * r).sum()) for r in ref)
+        cores = len(os.sched_getaffinity(0))
+        result["cpu_baseline"] = {"value": len(rows) / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+                                  "sample": f"direct definition with per-path mixing on {len(rows)} sampled output "
+                                            f"rows (b, i), fp64 numpy, {dt:.1f} s"}
+        result["parity_rel_l2_sampled_rows"] = (num / den) ** 0.5
+        log(f"[bench] mixed parity on {len(rows)} rows: rel_l2 = {result['parity_rel_l2_sampled_rows']:.3e}")
     else:
         result["cpu_baseline"] = None
     plan.close()

@@ -86,3 +86,26 @@ def cgconv_mixed_fft(q, k, L: int, W) -> np.ndarray:
         Uh = _mix_products(Pw, L, W)                                # (F, K, C)
         out[b] = np.fft.irfft(Uh, n=N, axis=0)
     return out
+
+
+def cgconv_mixed_direct_rows(q, k, L: int, W, rows) -> np.ndarray:
+    """Direct definition for selected output rows only; ``rows`` is a list of
+    (b, i).  Returns (len(rows), K, C) float64."""
+    q = np.asarray(q)
+    k = np.asarray(k)
+    if q.shape != k.shape or q.ndim != 4:
+        raise ValueError("q and k must both have shape (B, N, K, C)")
+    W = np.asarray(W, dtype=np.float64)
+    B, N, K, C = q.shape
+    if K != n_comp(L) or W.shape != (len(paths(L)), C, C):
+        raise ValueError("component axis or weight shape does not match L")
+    out = np.empty((len(rows), K, C))
+    for b in sorted({b for b, _ in rows}):
+        qb = q[b].astype(np.float64)
+        kb = k[b].astype(np.float64)
+        for n, (bb, i) in enumerate(rows):
+            if bb != b:
+                continue
+            kr = kb[(i - np.arange(N)) % N]
+            out[n] = _mix_products(np.einsum("jac,jbc->cab", qb, kr), L, W)
+    return out

@@ -131,3 +131,16 @@ def test_rejects_bad_weight_shape():
     with pytest.raises(ValueError):
         cgconv_mixed_direct(q, q, 1, np.zeros((len(paths(1)), 3, 2)))
     assert dense_R(1).shape == (4, 4, 4)
+
+
+def test_direct_rows_match_full_direct():
+    from oracle.mix import cgconv_mixed_direct_rows
+    rng = np.random.default_rng(40)
+    L, N, C = 2, 6, 3
+    q, k = _rand(rng, 2, N, L, C)
+    W = rng.normal(size=(len(paths(L)), C, C))
+    full = cgconv_mixed_direct(q, k, L, W)
+    rows = [(1, 5), (0, 0), (1, 2)]
+    got = cgconv_mixed_direct_rows(q, k, L, W, rows)
+    for n, (b, i) in enumerate(rows):
+        assert rel_l2(got[n], full[b, i]) < 1e-14
