@@ -179,3 +179,41 @@ def test_mixing_mistakes_are_caught(monkeypatch, plant):
             return out
         monkeypatch.setattr(omix, "_mix_products", bad)
     assert not _mix_pins_hold()
+
+
+@pytest.mark.parametrize("plant", ["softmax_over_channels", "squared_norm", "no_max_shift", "gate_on_v"])
+def test_gating_mistakes_are_caught(monkeypatch, plant):
+    import oracle.gate as og
+    orig_sm, orig_norm, orig_gate = og.softmax_tokens, og.invariant_norms, og.gate
+    if plant == "softmax_over_channels":
+        def bad(I):
+            e = np.exp(I - I.max(axis=3, keepdims=True))
+            return e / e.sum(axis=3, keepdims=True)
+        monkeypatch.setattr(og, "softmax_tokens", bad)
+    elif plant == "squared_norm":
+        monkeypatch.setattr(og, "invariant_norms", lambda u, L: orig_norm(u, L) ** 2)
+    elif plant == "no_max_shift":
+        monkeypatch.setattr(og, "softmax_tokens", lambda I: np.exp(I) / np.exp(I).sum(axis=1, keepdims=True))
+    else:
+        monkeypatch.setattr(og, "gate_value", lambda u, v, L: og.value_tensor_product(u, orig_gate(v, L), L))
+    caught = False
+    # the hand-computed gate values, the normalisation over tokens with large
+    # inputs, and the unit-scalar identity
+    L = 1
+    u = np.zeros((1, 2, 4, 1))
+    u[0, 0, 1:4, 0] = [0.0, 3.0, 0.0]
+    u[0, 1, 1:4, 0] = [2.4, 0.0, 3.2]
+    u[0, 0, 0, 0], u[0, 1, 0, 0] = -2.0, 0.5
+    from math import exp as _e
+    g = og.gate(u, L)
+    caught |= abs(g[0, 1, 3, 0] - 3.2 * _e(4) / (_e(3) + _e(4))) > 1e-12
+    rng = np.random.default_rng(5)
+    I = rng.normal(size=(2, 7, 3, 4)) * 800.0
+    with np.errstate(all="ignore"):
+        s = og.softmax_tokens(I)
+    caught |= not (np.all(np.isfinite(s)) and np.abs(s.sum(axis=1) - 1.0).max() < 1e-12)
+    uu = rng.normal(size=(1, 4, 9, 2))
+    vv = np.zeros_like(uu)
+    vv[:, :, 0, :] = 1.0
+    caught |= np.abs(og.gate_value(uu, vv, 2) - orig_gate(uu, 2)).max() > 1e-12
+    assert caught
