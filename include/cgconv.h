@@ -105,6 +105,23 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
                          float* out, hipStream_t stream);
 
 /*
+ * Invariant softmax gating and the real-space value tensor product (§4.2
+ * Invariant Gating; Algorithm 1, step 5), for the plan's batch, N, L_max, C:
+ *
+ *   I[b,i,l,c]     = || u[b,i,(l,.),c] ||_2          (norm over the 2l+1 components)
+ *   g[b,i,l,c]     = exp(I[b,i,l,c]) / sum_j exp(I[b,j,l,c])   (softmax over tokens)
+ *   f[b,i,(J,M),c] = sum_{paths} sum_{m1,m2} R^{(l1 l2 J)}[M,m1,m2]
+ *                    * g[b,i,l1,c] u[b,i,(l1,m1),c] * v[b,i,(l2,m2),c]
+ *
+ * (the paper leaves the invariant map gamma and the softmax axis open; these
+ * are the readings taken).  u (typically the convolution output), v (the
+ * values) and f: DEVICE pointers, fp32 [batch][N][(L_max+1)^2][C], 16-byte
+ * aligned; f must not alias u or v.  Uses a small plan-owned workspace; same
+ * stream rules as cgconv_forward.
+ */
+int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float* f, hipStream_t stream);
+
+/*
  * Host-only (no GPU needed): the CG paths at L_max in the order the mixing
  * weights use, every triangle-allowed (l1, l2, J) with l1, l2, J <= L_max
  * (odd l1+l2+J included), lexicographic in (l1, l2, J).  Writes up to cap

@@ -54,6 +54,8 @@ def library() -> ctypes.CDLL:
     lib.cgconv_forward_bf16.restype = ctypes.c_int
     lib.cgconv_forward_mixed.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.cgconv_forward_mixed.restype = ctypes.c_int
+    lib.cgconv_gate_value.argtypes = [vp, vp, vp, vp, vp]
+    lib.cgconv_gate_value.restype = ctypes.c_int
     lib.cgconv_paths.argtypes = [i32, ctypes.POINTER(i32), i64]
     lib.cgconv_paths.restype = i64
     lib.cgconv_plan_destroy.argtypes = [vp]
@@ -110,6 +112,11 @@ def cgconv_forward_bf16(plan: int, q: int, k: int, out: int, stream: int) -> int
 def cgconv_forward_mixed(plan: int, q: int, k: int, weights: int, out: int, stream: int) -> int:
     """Per-path channel mixing; weights: device fp32 [n_paths][C][C]."""
     return _check(library().cgconv_forward_mixed(plan, q, k, weights, out, stream))
+
+
+def cgconv_gate_value(plan: int, u: int, v: int, f: int, stream: int) -> int:
+    """Invariant softmax gating of u and its token-wise CG product with v."""
+    return _check(library().cgconv_gate_value(plan, u, v, f, stream))
 
 
 def cgconv_paths(L_max: int):
@@ -233,6 +240,16 @@ class Plan:
                 or tuple(weights.shape) != (P, C, C) or not weights.is_contiguous()):
             raise ValueError(f"weights must be a contiguous float32 GPU tensor of shape {(P, C, C)}")
         cgconv_forward_mixed(self._h, q.data_ptr(), k.data_ptr(), weights.data_ptr(), out.data_ptr(), s)
+        return out
+
+    def gate_value(self, u, v, out=None):
+        """Invariant softmax gating of u and the token-wise CG product with
+        v (fp32 tensors of the plan's shape)."""
+        import torch
+        if out is None:
+            out = torch.empty(self.shape, dtype=torch.float32, device=u.device)
+        s = self._args(u, v, out, torch.float32)
+        cgconv_gate_value(self._h, u.data_ptr(), v.data_ptr(), out.data_ptr(), s)
         return out
 
     __call__ = forward

@@ -66,6 +66,9 @@ def build(jobs: int | None = None, verbose: bool = True) -> str:
     for L in range(MIX_LMAX, -1, -1):
         units.append(([HIPCC, "-c"] + HIP_FLAGS, "cg_mix.hip", "cg_mix_L%d.o" % L,
                       ["-DCGCONV_TU_L=%d" % L, '-DCGCONV_BODY="cg_body_L%d.inc"' % L]))
+    for L in range(LGEN, -1, -1):
+        units.append(([HIPCC, "-c"] + HIP_FLAGS, "gate.hip", "gate_L%d.o" % L,
+                      ["-DCGCONV_TU_L=%d" % L, '-DCGCONV_BODY="cg_body_L%d.inc"' % L]))
     objs = []
 
     def compile_unit(u):

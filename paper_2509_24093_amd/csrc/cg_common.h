@@ -13,6 +13,8 @@ template <int L>
 struct CgBody;  // specialised by the generated cg_body_L<L>.inc files
 template <int L>
 struct CgPathBody;  // per-path variant for the channel-mixing kernel (same files)
+template <int L>
+struct CgRealBody;  // token-wise real-basis product of the value tensor product (same files)
 
 constexpr int kCgThreads = 256;
 

@@ -69,6 +69,8 @@ struct cgconv_plan {
   uint32_t* d_tkey = nullptr;
   float* d_tcoef = nullptr;
   uint16_t* d_wmix = nullptr;  // channel-mixing weights, split bf16 MFMA operands (L <= 6, C <= 32)
+  float2* d_gpart = nullptr;   // gating: online-softmax partials per token chunk
+  float2* d_gfin = nullptr;    // gating: maximum and denominator per (b, l, c)
   bool force_generic = false;
   // optional per-stage timing: events recorded on the forward's stream.  The
   // first timed call fixes the kind (plain or mixed) that is timed.
@@ -91,6 +93,8 @@ void free_plan(cgconv_plan* p) {
   (void)hipFree(p->d_tkey);
   (void)hipFree(p->d_tcoef);
   (void)hipFree(p->d_wmix);
+  (void)hipFree(p->d_gpart);
+  (void)hipFree(p->d_gfin);
   for (hipEvent_t ev : p->events) (void)hipEventDestroy(ev);
   (void)hipSetDevice(cur);
   delete p;
@@ -102,6 +106,21 @@ const char* const kStagesF[] = {"fft_fwd_1", "cg_fused", "fft_inv_2"};
 const char* const kStagesM2[] = {"fft_fwd_1", "fft_fwd_2", "cg_mix", "fft_inv_1", "fft_inv_2"};
 const char* const kStagesM1[] = {"fft_fwd", "cg_mix", "fft_inv"};
 constexpr int kMaxEvents = 6;  // stages + 1 of the longest pipeline
+
+hipError_t launch_gate(int L, const GateArgs& a, hipStream_t s) {
+  switch (L) {
+    case 0: return launch_gate_value<0>(a, s);
+    case 1: return launch_gate_value<1>(a, s);
+    case 2: return launch_gate_value<2>(a, s);
+    case 3: return launch_gate_value<3>(a, s);
+    case 4: return launch_gate_value<4>(a, s);
+    case 5: return launch_gate_value<5>(a, s);
+    case 6: return launch_gate_value<6>(a, s);
+    case 7: return launch_gate_value<7>(a, s);
+    case 8: return launch_gate_value<8>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_mix(int L, const CgArgs& a, hipStream_t s) {
   switch (L) {
@@ -431,6 +450,19 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
     free_plan(p);
     return nullptr;
   }
+  {
+    // gating partials: ceil(N / kGateChunk) chunks per batch element
+    const size_t chunks = (size_t)((N + kGateChunk - 1) / kGateChunk);
+    const size_t np = (size_t)batch * chunks * (L_max + 1) * C, nf = (size_t)batch * (L_max + 1) * C;
+    if ((e = hipMalloc(&p->d_gpart, np * sizeof(float2))) != hipSuccess ||
+        (e = hipMalloc(&p->d_gfin, nf * sizeof(float2))) != hipSuccess) {
+      set_error("gating workspace allocation failed: %s", hipGetErrorString(e));
+      (void)hipGetLastError();
+      free_plan(p);
+      return nullptr;
+    }
+    p->ws_bytes += (np + nf) * sizeof(float2);
+  }
   if (L_max <= kMixLmax && C <= kMixCmax) {
     // prepared channel-mixing weights, 2048 bf16 per path
     if ((e = hipMalloc(&p->d_wmix, (size_t)p->paths * 2048 * sizeof(uint16_t))) != hipSuccess) {
@@ -557,6 +589,26 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
     return CGCONV_ERR_UNSUPPORTED;
   }
   return run_forward(plan, q, k, out, false, stream, weights);
+}
+
+int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float* f, hipStream_t stream) {
+  const int st = check_forward_args(plan, u, v, f);
+  if (st != CGCONV_OK) return st;
+  GateArgs a;
+  a.u = u;
+  a.v = v;
+  a.f = f;
+  a.part = plan->d_gpart;
+  a.fin = plan->d_gfin;
+  a.B = (int)plan->B;
+  a.N = (int)plan->N;
+  a.C = (int)plan->C;
+  const hipError_t e = launch_gate(plan->L, a, stream);
+  if (e != hipSuccess) {
+    set_error("kernel launch failed: %s", hipGetErrorString(e));
+    return CGCONV_ERR_HIP;
+  }
+  return CGCONV_OK;
 }
 
 int64_t cgconv_paths(int32_t L_max, int32_t* l1l2J, int64_t cap) {

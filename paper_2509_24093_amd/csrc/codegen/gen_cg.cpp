@@ -33,7 +33,8 @@
 // a*(-b) and keeps a negated copy of every input alive for the whole kernel.
 //
 // A second body per L, CgPathBody<L>, keeps the paths apart for the
-// channel-mixing kernel (see emit_path_body).
+// channel-mixing kernel (see emit_path_body); a third, CgRealBody<L>, is the
+// token-wise real-basis product of the value tensor product (emit_real_body).
 //
 // Usage: gen_cg <output-dir> <LGEN>   (writes cg_body_L<L>.inc and cg_lgen.h)
 #include <algorithm>
@@ -407,6 +408,82 @@ void emit_path_body(FILE* f, int L, long* ops_out) {
   *ops_out = ops;
 }
 
+// Token-wise real-basis product for the value tensor product (CgRealBody<L>::run):
+//   f[J,M] = sum R^{(l1 l2 J)}[M,m1,m2] a[l1,m1] b[l2,m2]   (a, b, f real)
+// from the real-basis table.  The two ordered terms of a component pair
+// {x, y} (x != y) share one coefficient up to (-1)^(l1+l2-J) (the swap
+// symmetry, checked here for every pair), so per pair s = a_x b_y + a_y b_x
+// and/or d = a_x b_y - a_y b_x (2 ops each), then one FMA per coefficient;
+// a diagonal pair takes one product.
+void emit_real_body(FILE* f, int L, long* ops_out) {
+  const int K = (L + 1) * (L + 1);
+  std::vector<RealEntry> table = real_table(L);
+  std::map<std::pair<int, int>, std::vector<RealEntry>> by_pair;  // ordered (x, y) -> entries
+  for (const RealEntry& e : table) by_pair[{comp(e.l1, e.m1), comp(e.l2, e.m2)}].push_back(e);
+  long ops = 0;
+  std::set<int> inited;
+  std::fprintf(f, "template <>\nstruct CgRealBody<%d> {\n  static constexpr int K = %d;\n", L, K);
+  std::fprintf(f,
+               "  static __device__ __forceinline__ void run(const float (&a)[%d], const float (&b)[%d], "
+               "float (&f)[%d]) {\n",
+               K, K, K);
+  auto acc = [&](int o, double c, const char* src) {
+    if (!inited.count(o))
+      std::fprintf(f, "      f[%d] = %s * %s;\n", o, lit(c).c_str(), src);
+    else
+      std::fprintf(f, "      f[%d] = fmaf(%s, %s, f[%d]);\n", o, lit(c).c_str(), src, o);
+    inited.insert(o);
+    ++ops;
+  };
+  for (auto& kv : by_pair) {
+    const int x = kv.first.first, y = kv.first.second;
+    if (x > y) continue;  // handled with its partner
+    const std::vector<RealEntry>& ex = kv.second;
+    if (x == y) {
+      std::fprintf(f, "    { const float p = a[%d] * b[%d];\n", x, y);
+      ++ops;
+      for (const RealEntry& e : ex) acc(comp(e.J, e.M), e.coef, "p");
+      std::fprintf(f, "    }\n");
+      continue;
+    }
+    auto it = by_pair.find({y, x});
+    const std::vector<RealEntry> none;
+    const std::vector<RealEntry>& ey = it == by_pair.end() ? none : it->second;
+    bool ev = false, od = false;
+    for (const RealEntry& e : ex) {
+      const double sigma = ((e.l1 + e.l2 - e.J) % 2 == 0) ? 1.0 : -1.0;
+      const RealEntry* w = nullptr;
+      for (const RealEntry& z : ey)
+        if (z.J == e.J && z.M == e.M) w = &z;
+      if (!w || std::fabs(w->coef - sigma * e.coef) > 1e-12 * std::fabs(e.coef) + 1e-15) {
+        std::fprintf(stderr, "gen_cg: real swap symmetry violated (%d %d J=%d M=%d)\n", x, y, e.J, e.M);
+        std::exit(1);
+      }
+      (sigma > 0 ? ev : od) = true;
+    }
+    if (ex.size() != ey.size()) {
+      std::fprintf(stderr, "gen_cg: real swap partner count differs (%d %d)\n", x, y);
+      std::exit(1);
+    }
+    std::fprintf(f, "    {\n");
+    if (ev) {
+      std::fprintf(f, "      const float s = fmaf(a[%d], b[%d], a[%d] * b[%d]);\n", y, x, x, y);
+      ops += 2;
+    }
+    if (od) {
+      std::fprintf(f, "      const float d = fnma(a[%d], b[%d], a[%d] * b[%d]);\n", y, x, x, y);
+      ops += 2;
+    }
+    for (const RealEntry& e : ex) acc(comp(e.J, e.M), e.coef, ((e.l1 + e.l2 - e.J) % 2 == 0) ? "s" : "d");
+    std::fprintf(f, "    }\n");
+  }
+  for (int o = 0; o < K; ++o)
+    if (!inited.count(o)) std::fprintf(f, "    f[%d] = 0.f;\n", o);
+  std::fprintf(f, "  }\n");
+  std::fprintf(f, "  static constexpr long kOps = %ld;  // VALU ops per token and channel\n};\n\n", ops);
+  *ops_out = ops;
+}
+
 int main(int argc, char** argv) {
   if (argc != 3) {
     std::fprintf(stderr, "usage: %s <output-dir> <LGEN>\n", argv[0]);
@@ -423,11 +500,13 @@ int main(int argc, char** argv) {
     }
     std::fprintf(f, "// Generated by csrc/codegen/gen_cg.cpp -- do not edit.\n");
     std::fprintf(f, "// Frequency-domain CG contraction body, L_max = %d.\n#pragma once\n\n", L);
-    long ops = 0, pops = 0;
+    long ops = 0, pops = 0, rops = 0;
     emit_body(f, L, &ops);
     emit_path_body(f, L, &pops);
+    emit_real_body(f, L, &rops);
     std::fclose(f);
-    std::fprintf(stderr, "gen_cg: L=%d ops/point=%ld per-path ops/point=%ld\n", L, ops, pops);
+    std::fprintf(stderr, "gen_cg: L=%d ops/point=%ld per-path ops/point=%ld real token-wise ops=%ld\n", L, ops,
+                 pops, rops);
   }
   const std::string hpath = dir + "/cg_lgen.h";
   FILE* h = std::fopen(hpath.c_str(), "w");

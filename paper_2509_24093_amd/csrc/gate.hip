@@ -1,0 +1,181 @@
+// Invariant softmax gating and the real-space value tensor product for
+// gfx950 (arXiv 2509.24093, §4.2 Invariant Gating, Algorithm 1 step 5).
+// Built once per L_max (-DCGCONV_TU_L, -DCGCONV_BODY):
+//
+//   I[b,i,l,c] = || u[b,i,(l,.),c] ||_2                     per-degree norm
+//   g[b,i,l,c] = exp(I[b,i,l,c]) / sum_j exp(I[b,j,l,c])     softmax over tokens
+//   f[b,i,(J,M),c] = sum R^{(l1 l2 J)}[M,m1,m2] g[b,i,l1,c] u[b,i,(l1,m1),c]
+//                                              v[b,i,(l2,m2),c]
+//
+// Three kernels: (1) each block reduces a chunk of kGateChunk tokens of one
+// batch element to online-softmax partials (running maximum m and sum of
+// exp(I - m)) per (l, c); (2) the partials of all chunks are combined into
+// the maximum and denominator per (b, l, c); (3) one lane per (b, i, c)
+// recomputes its norms, applies the gate and evaluates the generated
+// token-wise real-basis product (CgRealBody).  u, v, f: fp32 [B][N][K][C],
+// channel fastest, so every load and store of a wave is contiguous.
+#include <hip/hip_runtime.h>
+
+#include "cg_common.h"
+
+namespace cgconv {
+namespace cgdev {
+#include CGCONV_BODY
+}  // namespace cgdev
+
+namespace {
+
+using namespace cgdev;
+
+constexpr int kGateThreads = 256;
+
+template <int L>
+__device__ __forceinline__ void degree_norms(const float* x, float (&I)[L + 1]) {
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
+    float s = 0.f;
+#pragma unroll
+    for (int m = 0; m < 2 * l + 1; ++m) s = fmaf(x[l * l + m], x[l * l + m], s);
+    I[l] = __builtin_sqrtf(s);
+  }
+}
+
+// Block (chunk, b, channel group): threads = (token slot ts, channel c), c
+// fastest; every thread walks the chunk's tokens ts, ts + TS, ...
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gate_partials_kernel(const float* __restrict__ u,
+                                                                     float2* __restrict__ part, int N, int C,
+                                                                     int chunks) {
+  constexpr int K = (L + 1) * (L + 1);
+  __shared__ float2 red[kGateThreads][L + 1];
+  const int cpb = C < kGateThreads ? C : kGateThreads;  // channels per block
+  const int TS = kGateThreads / cpb;                    // token slots per block
+  const int tid = threadIdx.x;
+  const int c = blockIdx.z * cpb + tid % cpb, ts = tid / cpb;
+  const bool active = ts < TS && c < C && tid < TS * cpb;
+  const int chunk = blockIdx.x, b = blockIdx.y;
+  float mx[L + 1], sm[L + 1];
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
+    mx[l] = -INFINITY;
+    sm[l] = 0.f;
+  }
+  if (active) {
+    const int i_end = min(N, (chunk + 1) * kGateChunk);
+    for (int i = chunk * kGateChunk + ts; i < i_end; i += TS) {
+      const float* x = u + ((long long)b * N + i) * K * C + c;
+      float xv[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) xv[k] = x[(long long)k * C];
+      float I[L + 1];
+      degree_norms<L>(xv, I);
+#pragma unroll
+      for (int l = 0; l <= L; ++l) {  // online softmax: keep sum exp(I - max)
+        if (I[l] > mx[l]) {
+          sm[l] = sm[l] * __expf(mx[l] - I[l]) + 1.f;
+          mx[l] = I[l];
+        } else {
+          sm[l] += __expf(I[l] - mx[l]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int l = 0; l <= L; ++l) red[tid][l] = make_float2(mx[l], sm[l]);
+  __syncthreads();
+  if (active && ts == 0) {
+#pragma unroll
+    for (int l = 0; l <= L; ++l) {
+      float m = -INFINITY, s = 0.f;
+      for (int t = 0; t < TS; ++t) {
+        const float2 p = red[t * cpb + tid % cpb][l];
+        if (p.y == 0.f) continue;
+        const float nm = fmaxf(m, p.x);
+        s = s * __expf(m - nm) + p.y * __expf(p.x - nm);
+        m = nm;
+      }
+      part[(((long long)b * chunks + chunk) * (L + 1) + l) * C + c] = make_float2(m, s);
+    }
+  }
+}
+
+// One thread per (b, l, c): combine the chunks' partials.
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gate_finalize_kernel(const float2* __restrict__ part,
+                                                                     float2* __restrict__ fin, int B, int C,
+                                                                     int chunks) {
+  const long long t = (long long)blockIdx.x * kGateThreads + threadIdx.x;
+  if (t >= (long long)B * (L + 1) * C) return;
+  const int c = (int)(t % C);
+  const int l = (int)((t / C) % (L + 1));
+  const long long b = t / ((long long)C * (L + 1));
+  float m = -INFINITY, s = 0.f;
+  for (int k = 0; k < chunks; ++k) {
+    const float2 p = part[((b * chunks + k) * (L + 1) + l) * C + c];
+    if (p.y == 0.f) continue;
+    const float nm = fmaxf(m, p.x);
+    s = s * __expf(m - nm) + p.y * __expf(p.x - nm);
+    m = nm;
+  }
+  fin[t] = make_float2(m, s);  // [b][l][c]: maximum, denominator
+}
+
+// One lane per (b, i, c), c fastest.
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gate_value_kernel(const float* __restrict__ u,
+                                                                  const float* __restrict__ v,
+                                                                  const float2* __restrict__ fin,
+                                                                  float* __restrict__ f, int N, int C,
+                                                                  long long lanes) {
+  constexpr int K = (L + 1) * (L + 1);
+  const long long p = (long long)blockIdx.x * kGateThreads + threadIdx.x;
+  if (p >= lanes) return;
+  const int c = (int)(p % C);
+  const long long bi = p / C;  // b * N + i
+  const long long b = bi / N;
+  const float* x = u + bi * K * C + c;
+  const float* y = v + bi * K * C + c;
+  float a[K], w[K], out[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    a[k] = x[(long long)k * C];
+    w[k] = y[(long long)k * C];
+  }
+  float I[L + 1];
+  degree_norms<L>(a, I);
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
+    const float2 ms = fin[(b * (L + 1) + l) * C + c];
+    const float g = __expf(I[l] - ms.x) / ms.y;
+#pragma unroll
+    for (int m = 0; m < 2 * l + 1; ++m) a[l * l + m] *= g;
+  }
+  CgRealBody<L>::run(a, w, out);
+  float* z = f + bi * K * C + c;
+#pragma unroll
+  for (int k = 0; k < K; ++k) z[(long long)k * C] = out[k];
+}
+
+}  // namespace
+
+template <>
+hipError_t launch_gate_value<CGCONV_TU_L>(const GateArgs& a, hipStream_t s) {
+  if (a.B < 1 || a.N < 1 || a.C < 1 || !a.u || !a.v || !a.f || !a.part || !a.fin) return hipErrorInvalidValue;
+  const int chunks = (a.N + kGateChunk - 1) / kGateChunk;
+  const int cpb = a.C < kGateThreads ? a.C : kGateThreads;
+  const dim3 g1(chunks, a.B, (a.C + cpb - 1) / cpb);
+  hipLaunchKernelGGL(gate_partials_kernel<CGCONV_TU_L>, g1, dim3(kGateThreads), 0, s, a.u, a.part, a.N, a.C,
+                     chunks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const long long nf = (long long)a.B * (CGCONV_TU_L + 1) * a.C;
+  hipLaunchKernelGGL(gate_finalize_kernel<CGCONV_TU_L>, dim3((unsigned)((nf + kGateThreads - 1) / kGateThreads)),
+                     dim3(kGateThreads), 0, s, a.part, a.fin, a.B, a.C, chunks);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const long long lanes = (long long)a.B * a.N * a.C;
+  hipLaunchKernelGGL(gate_value_kernel<CGCONV_TU_L>, dim3((unsigned)((lanes + kGateThreads - 1) / kGateThreads)),
+                     dim3(kGateThreads), 0, s, a.u, a.v, a.fin, a.f, a.N, a.C, lanes);
+  return hipGetLastError();
+}
+
+}  // namespace cgconv

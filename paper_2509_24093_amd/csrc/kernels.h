@@ -99,6 +99,22 @@ constexpr int kMixCmax = 32;
 // order above (4 KiB per path), zero outside C x C.
 hipError_t launch_prepare_mix_weights(const float* W, uint16_t* wt, int paths, int C, hipStream_t s);
 
+// Invariant softmax gating + real-space value tensor product (gate.hip), one
+// specialisation per L_max: u, v, f fp32 [B][N][K][C]; part holds
+// B * ceil(N / kGateChunk) * (L+1) * C online-softmax partials (maximum,
+// sum of exp), fin B * (L+1) * C combined ones.
+constexpr int kGateChunk = 64;
+struct GateArgs {
+  const float* u;
+  const float* v;
+  float* f;
+  float2* part;
+  float2* fin;
+  int B, N, C;
+};
+template <int L>
+hipError_t launch_gate_value(const GateArgs& a, hipStream_t s);
+
 // Fused second forward pass + CG stage + first inverse pass for two-pass
 // plans with N2 = 64 (see cg_fused.hip).  Y: output of the first forward
 // pass, class w1 at rows w1*64 + n2; V: input of the last inverse pass,

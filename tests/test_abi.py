@@ -124,3 +124,8 @@ def test_mixed_entry_points_reject_bad_arguments():
     buf = (ctypes.c_int32 * 6)(*([-7] * 6))
     n = lib.cgconv_paths(2, buf, 2)
     assert n == 15 and buf[5] != -7
+
+
+def test_gate_entry_point_rejects_null_plan():
+    lib = P.library()
+    assert lib.cgconv_gate_value(None, 16, 32, 48, None) == P.CGCONV_ERR_INVALID_ARG
