@@ -11,9 +11,10 @@ resident in HBM.
 
 Prints ONE JSON line.  Besides the contract fields it carries
   roofline      the dominant kernel (the CG stage, VALU-bound) against the
-                fp32 FMA issue rate, timed live with HIP events on the stream
-                the kernels run on; traffic from the committed rocprofv3
-                counter summary if it was taken on the current kernel source
+                fp32 vector peak (157.3 TFLOP/s), timed live with HIP
+                events on the stream the kernels run on; traffic from the
+                committed rocprofv3 counter summary if it was taken on the
+                current kernel source
   stages        per-stage average time and achieved bandwidth of each kernel
   cpu_baseline  the CPU oracle (direct O(N^2) definition) on sampled output
                 rows of the same inputs; those rows also check the GPU output
@@ -23,7 +24,10 @@ workloads, for exploration), --bf16, --copy-calibration (a plain device copy
 of known size, the reference for rocprofv3 byte counters), --mixed (the
 convolution with per-path channel mixing, cgconv_forward_mixed, with seeded
 random weights: its own JSON line, the mixing stage against the bf16 matrix
-core peak).
+core peak), --backward (cgconv_backward, both gradients, for a seeded
+output gradient: its own JSON line), --gate (cgconv_gate_value with the
+workload's q and k as u and v: its own JSON line, gate_value against the
+fp32 vector peak).
 """
 
 from __future__ import annotations
@@ -39,13 +43,15 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
-# fp32 FMA issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz.  The
-# published 157.3 TFLOP/s "vector fp32" counts packed-fp32 dual issue, which
-# this build does not use (packed fp32 instructions are disabled).
-VALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
-VALU_PEAK_PACKED_TFLOPS = 157.3
+# fp32 vector peak: 256 CUs x 4 SIMDs x 32 lanes per cycle x 2 flop x 2.4 GHz.
+# A SIMD completes one wave64 fp32 FMA (v_fmac_f32, not packed) every 2
+# cycles when two or more waves are ready; one wave alone issues at most one
+# every 4 cycles, i.e. half this rate.
+VALU_PEAK_TFLOPS = 256 * 4 * 32 * 2 * 2.4e9 / 1e12
 METRIC = "CG-conv tokens/sec at N=16384, L_max=6, C=32; achieved HBM GB/s vs peak"
 METRIC_MIXED = "CG-conv with per-path channel mixing, tokens/sec at N=16384, L_max=6, C=32"
+METRIC_BACKWARD = "CG-conv backward (grad_q and grad_k), tokens/sec at N=16384, L_max=6, C=32"
+METRIC_GATE = "invariant softmax gating + value tensor product, tokens/sec at N=16384, L_max=6, C=32"
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
 CG_SOURCES = ["paper_2509_24093_amd/csrc/cg_gen.hip", "paper_2509_24093_amd/csrc/cg_fused.hip",
               "paper_2509_24093_amd/csrc/cg_common.h", "paper_2509_24093_amd/csrc/fft_reg.h",
@@ -141,6 +147,43 @@ def cpu_baseline(q, k, L, budget_s, got):
     return obj, (num / den) ** 0.5 if den > 0 else 0.0, R
 
 
+def cg_roofline(stage_avg, B, N, L, C, n_products, nnz, traffic, traffic_src):
+    """Roofline object of the CG stage (fused or unfused) from its average
+    launch time: algorithmic flops per launch against the fp32 vector peak."""
+    K = (L + 1) ** 2
+    Cp = (C + 1) // 2
+    F = N // 2 + 1
+    points = B * F * C
+    cg_flops_per_point = 6 * n_products + 4 * nnz
+    dom = "cg_fused" if "cg_fused" in stage_avg else "cg"
+    cg_ms = stage_avg[dom]
+    flops = points * cg_flops_per_point
+    flop_model = (f"(6*{n_products} distinct complex products + 4*{nnz} non-zeros) per "
+                  f"(b, frequency 0..N/2, channel) point, {points} points")
+    if dom == "cg_fused":
+        # the fused kernel also runs the length-64 DFTs over n2: 5 n log2 n
+        # flops per complex transform, K*C forward and K*ceil(C/2) inverse
+        # columns per class
+        n1 = N // 64
+        dft = 5 * 64 * 6
+        flops += dft * B * n1 * K * (C + Cp)
+        flop_model += f" + {dft}-flop length-64 DFTs on {B * n1 * K * (C + Cp)} columns"
+    achieved_tflops = flops / (cg_ms * 1e-3) / 1e12
+    return {
+        "kernel": f"{'cg_fused_kernel' if dom == 'cg_fused' else 'cg_gen_kernel'}<{L}>",
+        "bound": "alu",
+        "achieved": round(achieved_tflops, 2),
+        "peak": round(VALU_PEAK_TFLOPS, 1),
+        "unit": "TFLOP/s",
+        "frac": round(achieved_tflops / VALU_PEAK_TFLOPS, 4),
+        "traffic": traffic,
+        "traffic_source": traffic_src,
+        "flops_per_launch": flops,
+        "flop_model": flop_model,
+        "launch_ms": round(cg_ms, 4),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -152,6 +195,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--mixed", action="store_true")
+    ap.add_argument("--backward", action="store_true")
+    ap.add_argument("--gate", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: this build runs on one GPU only "
@@ -190,6 +235,12 @@ def main():
     if args.mixed:
         bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C)
         return
+    if args.backward:
+        bench_backward(args, plan, q, k, qd, kd, B, N, L, C)
+        return
+    if args.gate:
+        bench_gate(args, plan, q, k, qd, kd, out, B, N, L, C)
+        return
     n_paths, nnz, n_products, ws_bytes = plan.info()
     log(f"[bench] plan: paths={n_paths} nnz={nnz} products={n_products} workspace={ws_bytes / 2**30:.2f} GiB")
 
@@ -222,39 +273,9 @@ def main():
         io = {"fft_fwd": 2 * S + 2 * Sc, "cg": 2 * Sc + Sp, "fft_inv": Sp + S}
     stages = {s: {"ms": round(t, 4), "bytes": io.get(s), "gbs": round(io.get(s, 0) / (t * 1e-3) / 1e9, 1)}
               for s, t in stage_avg.items()}
-    F = N // 2 + 1
-    points = B * F * C
-    cg_flops_per_point = 6 * n_products + 4 * nnz
-    dom = "cg_fused" if "cg_fused" in stage_avg else "cg"
-    cg_ms = stage_avg[dom]
-    flops = points * cg_flops_per_point
-    flop_model = (f"(6*{n_products} distinct complex products + 4*{nnz} non-zeros) per "
-                  f"(b, frequency 0..N/2, channel) point, {points} points")
-    if dom == "cg_fused":
-        # the fused kernel also runs the length-64 DFTs over n2: 5 n log2 n
-        # flops per complex transform, K*C forward and K*ceil(C/2) inverse
-        # columns per class
-        n1 = N // 64
-        dft = 5 * 64 * 6
-        flops += dft * B * n1 * K * (C + Cp)
-        flop_model += f" + {dft}-flop length-64 DFTs on {B * n1 * K * (C + Cp)} columns"
-    achieved_tflops = flops / (cg_ms * 1e-3) / 1e12
     counters, traffic_src = committed_counters(args.workload) if not args.bf16 else (None, "bf16 run")
-    traffic = counters["cg_hbm_bytes_per_launch"] if counters else None
-    roofline = {
-        "kernel": f"{'cg_fused_kernel' if dom == 'cg_fused' else 'cg_gen_kernel'}<{L}>",
-        "bound": "alu",
-        "achieved": round(achieved_tflops, 2),
-        "peak": round(VALU_PEAK_TFLOPS, 1),
-        "unit": "TFLOP/s",
-        "frac": round(achieved_tflops / VALU_PEAK_TFLOPS, 4),
-        "traffic": traffic,
-        "traffic_source": traffic_src,
-        "flops_per_launch": flops,
-        "flop_model": flop_model,
-        "launch_ms": round(cg_ms, 4),
-        "frac_of_packed_fp32_peak": round(achieved_tflops / VALU_PEAK_PACKED_TFLOPS, 4),
-    }
+    roofline = cg_roofline(stage_avg, B, N, L, C, n_products, nnz,
+                           counters["cg_hbm_bytes_per_launch"] if counters else None, traffic_src)
     hbm_alg_gbs = 3 * S / (ms * 1e-3) / 1e9
     result = {
         "metric": METRIC,
@@ -381,6 +402,147 @@ def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
                                             f"rows (b, i), fp64 numpy, {dt:.1f} s"}
         result["parity_rel_l2_sampled_rows"] = (num / den) ** 0.5
         log(f"[bench] mixed parity on {len(rows)} rows: rel_l2 = {result['parity_rel_l2_sampled_rows']:.3e}")
+    else:
+        result["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(result), flush=True)
+
+
+def _common(args, metric, ms, B, N, L, C, dtype):
+    return {"metric": metric, "value": B * N / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+            "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C,
+                       "parallelism": "single GPU"}}
+
+
+def _timed(args, step, plan, calls_per_step=1):
+    """Warm up, then time args.steps calls of step() with the plan's stage
+    timing on; returns (ms per step, {stage: average ms per timed call})."""
+    import torch
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    plan.enable_timing(args.steps * calls_per_step)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    stage_ms, ncalls = plan.stage_times()
+    return ms, {s: v / max(ncalls, 1) for s, v in stage_ms.items()}
+
+
+def bench_backward(args, plan, q, k, qd, kd, B, N, L, C):
+    """cgconv_backward (both gradients) for a seeded output gradient ~ N(0, 1).
+    Each gradient is one forward-shaped pipeline on the same kernels, so the
+    stage times are averages over the 2 * steps pipelines."""
+    import numpy as np
+    import torch
+
+    import paper_2509_24093_amd as P
+    g = np.random.default_rng(2027).normal(size=q.shape).astype(np.float32)
+    gd = torch.from_numpy(g).cuda()
+    gq, gk = torch.empty_like(qd), torch.empty_like(qd)
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step():
+        P.cgconv_backward(plan._h, qd.data_ptr(), kd.data_ptr(), gd.data_ptr(), gq.data_ptr(), gk.data_ptr(),
+                          stream)
+    log(f"[bench] timing {args.steps} backward steps")
+    ms, stage_avg = _timed(args, step, plan, calls_per_step=2)
+    _, nnz, n_products, _ = plan.info()
+    counters, src = committed_counters(args.workload)
+    roofline = cg_roofline(stage_avg, B, N, L, C, n_products, nnz,
+                           counters["cg_hbm_bytes_per_launch"] if counters else None,
+                           (src + "; taken on the forward, same kernel and launch shape") if counters else src)
+    result = _common(args, METRIC_BACKWARD, ms, B, N, L, C, "f32")
+    result["roofline"] = roofline
+    result["stages_per_gradient"] = {s: {"ms": round(t, 4)} for s, t in stage_avg.items()}
+    if not args.no_cpu_baseline:
+        from oracle.backward import backward_direct_rows
+        log(f"[bench] CPU oracle baseline, backward (~{args.cpu_seconds:.0f} s)")
+        got = {"q": gq.cpu().numpy(), "k": gk.cpu().numpy()}
+        rng = np.random.default_rng(2028)
+        rows, num, den = [], 0.0, 0.0
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_seconds or len(rows) < 2:
+            b = len(rows) % B
+            part = [(b, 0 if not rows else int(rng.integers(0, N)))]
+            for wrt in ("q", "k"):
+                ref = backward_direct_rows(q, k, g, L, part, wrt)[0]
+                d = got[wrt][part[0]].astype(np.float64) - ref
+                num += float((d * d).sum())
+                den += float((ref * ref).sum())
+            rows.extend(part)
+        dt = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": len(rows) / dt, "unit": "tokens/s", "cores": len(os.sched_getaffinity(0)),
+                                  "kind": "oracle",
+                                  "sample": f"direct sums of both gradients on {len(rows)} sampled rows (b, j), "
+                                            f"all components and channels, fp64 numpy, {dt:.1f} s"}
+        result["parity_rel_l2_sampled_rows"] = (num / den) ** 0.5
+        log(f"[bench] backward parity on {len(rows)} rows: rel_l2 = {result['parity_rel_l2_sampled_rows']:.3e}")
+    else:
+        result["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(result), flush=True)
+
+
+def bench_gate(args, plan, q, k, qd, kd, out, B, N, L, C):
+    """cgconv_gate_value with u = q and v = k of the workload."""
+    import numpy as np
+
+    import paper_2509_24093_amd as P
+    log(f"[bench] timing {args.steps} gating steps")
+    ms, stage_avg = _timed(args, lambda: plan.gate_value(qd, kd, out), plan)
+    K = (L + 1) ** 2
+    _, coef = P.cgconv_cg_table(L)
+    nnz_real = len(coef)
+    lanes = B * N * C
+    per_lane = K * K + 2 * nnz_real + 3 * K
+    flops = per_lane * lanes
+    gv_ms = stage_avg["gate_value"]
+    achieved = flops / (gv_ms * 1e-3) / 1e12
+    result = _common(args, METRIC_GATE, ms, B, N, L, C, "f32")
+    result["roofline"] = {
+        "kernel": f"gate_value_kernel<{L}>",
+        "bound": "alu",
+        "achieved": round(achieved, 2),
+        "peak": round(VALU_PEAK_TFLOPS, 1),
+        "unit": "TFLOP/s",
+        "frac": round(achieved / VALU_PEAK_TFLOPS, 4),
+        "traffic": None,
+        "flops_per_launch": flops,
+        "flop_model": (f"per (b, i, c) lane: {K}^2 products u_x v_y + 2 flops (multiply-add by the "
+                       f"coefficient) per real-basis non-zero ({nnz_real}) + 3K for the norms and the gate; "
+                       f"{lanes} lanes"),
+        "algorithmic_bytes_per_launch": 3 * K * 4 * lanes,
+        "achieved_gbs": round(3 * K * 4 * lanes / (gv_ms * 1e-3) / 1e9, 1),
+        "launch_ms": round(gv_ms, 4),
+    }
+    result["stages"] = {s: {"ms": round(t, 4)} for s, t in stage_avg.items()}
+    if not args.no_cpu_baseline:
+        from oracle.gate import gate_value
+        log(f"[bench] CPU oracle baseline, gating (~{args.cpu_seconds:.0f} s)")
+        got = out.cpu().numpy()
+        num = den = 0.0
+        chans = []
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_seconds and len(chans) < C:
+            c = len(chans)
+            ref = gate_value(q[0:1, :, :, c:c + 1], k[0:1, :, :, c:c + 1], L)
+            d = got[0:1, :, :, c:c + 1].astype(np.float64) - ref
+            num += float((d * d).sum())
+            den += float((ref * ref).sum())
+            chans.append(c)
+        dt = time.perf_counter() - t0
+        tokens = N * len(chans) / C
+        result["cpu_baseline"] = {"value": tokens / dt, "unit": "tokens/s", "cores": len(os.sched_getaffinity(0)),
+                                  "kind": "oracle",
+                                  "sample": f"batch element 0, all {N} tokens, channels 0..{len(chans) - 1} of {C} "
+                                            f"({tokens:.0f} token-equivalents), fp64 numpy, {dt:.1f} s"}
+        result["parity_rel_l2_sampled_channels"] = (num / den) ** 0.5
+        log(f"[bench] gating parity on {len(chans)} channels: rel_l2 = {result['parity_rel_l2_sampled_channels']:.3e}")
     else:
         result["cpu_baseline"] = None
     plan.close()

@@ -96,13 +96,40 @@ int cgconv_forward_bf16(cgconv_plan_t plan, const uint16_t* q, const uint16_t* k
  * weights: DEVICE pointer, fp32 [n_paths][C][C] (row = output channel c,
  * column = input channel c'), 16-byte aligned, paths in the order of
  * cgconv_paths.  W_p = identity for every p gives cgconv_forward.  q, k, out
- * as for cgconv_forward (fp32).  The dense mixing runs on the matrix cores
- * (fp32 MFMA); the unfused FFT passes are used.  Needs L_max <= 6 and C <= 32
+ * as for cgconv_forward (fp32).  The dense mixing runs on the bfloat16
+ * matrix cores with both operands split into bfloat16 high and low parts
+ * (three products per tile, fp32 accumulation; relative error about 2^-17
+ * per product); the unfused FFT passes are used.  Needs L_max <= 6 and C <= 32
  * (CGCONV_ERR_UNSUPPORTED otherwise).  Same stream and workspace rules as
  * cgconv_forward; the weights are read during the call only.
  */
 int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, const float* weights,
                          float* out, hipStream_t stream);
+
+/*
+ * Backward of cgconv_forward (the models of §5 are trained by gradient
+ * descent through this operation): given grad_out = dL/dout for a scalar L,
+ *
+ *   grad_q[b,j,(l1,m1),c] = sum_i sum_{J,M,l2,m2} R^{(l1 l2 J)}[M,m1,m2]
+ *                           * grad_out[b,i,(J,M),c] * k[b,(i-j) mod N,(l2,m2),c]
+ *   grad_k[b,n,(l2,m2),c] = sum_i sum_{J,M,l1,m1} R^{(l1 l2 J)}[M,m1,m2]
+ *                           * grad_out[b,i,(J,M),c] * q[b,(i-n) mod N,(l1,m1),c]
+ *
+ * (cyclic correlations with the transposed tensor).  Computed as two
+ * forward convolutions on the same kernels: per path the real-basis tensor
+ * satisfies R^{(J l2 l1)}[m1,M,m2] = (-1)^l2 sqrt((2 l1+1)/(2J+1))
+ * R^{(l1 l2 J)}[M,m1,m2], so grad_q = s_o * conv(s_a * grad_out, s_b *
+ * reverse(k)) with per-degree scales and reverse(x)[n] = x[-n mod N], and
+ * likewise grad_k.  q, k, grad_out: DEVICE pointers, fp32, the layout of
+ * cgconv_forward; grad_q, grad_k: outputs of the same layout, either may be
+ * NULL (that gradient is skipped), not both; they must not alias q, k,
+ * grad_out or each other.  q == k is allowed: the gradient with respect to
+ * the shared tensor is then grad_q + grad_k (the caller adds them).  Same
+ * stream and workspace rules as cgconv_forward; the two gradients are
+ * computed one after the other in the plan's workspace.
+ */
+int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const float* grad_out,
+                    float* grad_q, float* grad_k, hipStream_t stream);
 
 /*
  * Invariant softmax gating and the real-space value tensor product (§4.2
@@ -175,8 +202,11 @@ int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, 
  * fft_fwd, cg, fft_inv; 5 above: fft_fwd_1, fft_fwd_2, cg, fft_inv_1,
  * fft_inv_2; for plans with 512 <= N <= 16384 and L_max <= 6: fft_fwd_1,
  * cg_fused, fft_inv_2) and the number of timed calls.  The first timed call
- * fixes whether plain or mixed forwards are timed (mixed: cg_mix replaces cg
- * and the unfused passes are listed); calls of the other kind are not timed.
+ * fixes which kind is timed: plain forwards, mixed forwards (cg_mix replaces
+ * cg and the unfused passes are listed), backwards (each of the two
+ * gradients is one timed call with the plain stages) or gating calls
+ * (gate_partials, gate_finalize, gate_value); calls of the other kinds are
+ * not timed.
  * cgconv_plan_stage_name returns a stage's name ("" if out of range).
  */
 int cgconv_plan_enable_timing(cgconv_plan_t plan, int32_t max_calls);

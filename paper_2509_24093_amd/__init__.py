@@ -54,6 +54,8 @@ def library() -> ctypes.CDLL:
     lib.cgconv_forward_bf16.restype = ctypes.c_int
     lib.cgconv_forward_mixed.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.cgconv_forward_mixed.restype = ctypes.c_int
+    lib.cgconv_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    lib.cgconv_backward.restype = ctypes.c_int
     lib.cgconv_gate_value.argtypes = [vp, vp, vp, vp, vp]
     lib.cgconv_gate_value.restype = ctypes.c_int
     lib.cgconv_paths.argtypes = [i32, ctypes.POINTER(i32), i64]
@@ -112,6 +114,12 @@ def cgconv_forward_bf16(plan: int, q: int, k: int, out: int, stream: int) -> int
 def cgconv_forward_mixed(plan: int, q: int, k: int, weights: int, out: int, stream: int) -> int:
     """Per-path channel mixing; weights: device fp32 [n_paths][C][C]."""
     return _check(library().cgconv_forward_mixed(plan, q, k, weights, out, stream))
+
+
+def cgconv_backward(plan: int, q: int, k: int, grad_out: int, grad_q, grad_k, stream: int) -> int:
+    """Gradients of a scalar loss with respect to q and k given grad_out
+    (device pointers; grad_q or grad_k may be None to skip it)."""
+    return _check(library().cgconv_backward(plan, q, k, grad_out, grad_q, grad_k, stream))
 
 
 def cgconv_gate_value(plan: int, u: int, v: int, f: int, stream: int) -> int:
@@ -252,6 +260,22 @@ class Plan:
         cgconv_gate_value(self._h, u.data_ptr(), v.data_ptr(), out.data_ptr(), s)
         return out
 
+    def backward(self, q, k, grad_out, need_q: bool = True, need_k: bool = True):
+        """(grad_q, grad_k) of a scalar loss given grad_out = dL/dout (fp32);
+        a gradient that is not needed is returned as None."""
+        import torch
+        if not (need_q or need_k):
+            return None, None
+        gq = torch.empty(self.shape, dtype=torch.float32, device=q.device) if need_q else None
+        gk = torch.empty(self.shape, dtype=torch.float32, device=q.device) if need_k else None
+        s = self._args(q, k, grad_out, torch.float32)
+        for name, t in (("grad_q", gq), ("grad_k", gk)):
+            if t is not None:
+                self._args(t, t, t, torch.float32)
+        cgconv_backward(self._h, q.data_ptr(), k.data_ptr(), grad_out.data_ptr(),
+                        gq.data_ptr() if gq is not None else None, gk.data_ptr() if gk is not None else None, s)
+        return gq, gk
+
     __call__ = forward
 
     def close(self):
@@ -264,3 +288,31 @@ class Plan:
             self.close()
         except Exception:
             pass
+
+
+_autograd_fn = None
+
+
+def cgconv(q, k, plan: Plan):
+    """Differentiable CG convolution of fp32 tensors: the forward and the
+    backward are the plan's cgconv_forward and cgconv_backward."""
+    global _autograd_fn
+    if _autograd_fn is None:
+        import torch
+
+        class _CgconvFn(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, q, k, plan):
+                ctx.save_for_backward(q, k)
+                ctx.plan = plan
+                return plan.forward(q, k)
+
+            @staticmethod
+            def backward(ctx, grad_out):
+                q, k = ctx.saved_tensors
+                gq, gk = ctx.plan.backward(q, k, grad_out.contiguous(), need_q=ctx.needs_input_grad[0],
+                                           need_k=ctx.needs_input_grad[1])
+                return gq, gk, None
+
+        _autograd_fn = _CgconvFn
+    return _autograd_fn.apply(q, k, plan)

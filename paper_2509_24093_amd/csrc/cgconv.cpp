@@ -71,6 +71,7 @@ struct cgconv_plan {
   uint16_t* d_wmix = nullptr;  // channel-mixing weights, split bf16 MFMA operands (L <= 6, C <= 32)
   float2* d_gpart = nullptr;   // gating: online-softmax partials per token chunk
   float2* d_gfin = nullptr;    // gating: maximum and denominator per (b, l, c)
+  float* d_bscale = nullptr;   // backward: per-component scales, [2 gradients][in a, in b, out][K]
   bool force_generic = false;
   // optional per-stage timing: events recorded on the forward's stream.  The
   // first timed call fixes the kind (plain or mixed) that is timed.
@@ -95,6 +96,7 @@ void free_plan(cgconv_plan* p) {
   (void)hipFree(p->d_wmix);
   (void)hipFree(p->d_gpart);
   (void)hipFree(p->d_gfin);
+  (void)hipFree(p->d_bscale);
   for (hipEvent_t ev : p->events) (void)hipEventDestroy(ev);
   (void)hipSetDevice(cur);
   delete p;
@@ -105,6 +107,9 @@ const char* const kStages1[] = {"fft_fwd", "cg", "fft_inv"};
 const char* const kStagesF[] = {"fft_fwd_1", "cg_fused", "fft_inv_2"};
 const char* const kStagesM2[] = {"fft_fwd_1", "fft_fwd_2", "cg_mix", "fft_inv_1", "fft_inv_2"};
 const char* const kStagesM1[] = {"fft_fwd", "cg_mix", "fft_inv"};
+const char* const kStagesG[] = {"gate_partials", "gate_finalize", "gate_value"};
+// timing kinds: 0 forward, 1 mixed forward, 2 backward (each gradient one call), 3 gating
+constexpr int kKindGate = 3;
 constexpr int kMaxEvents = 6;  // stages + 1 of the longest pipeline
 
 hipError_t launch_gate(int L, const GateArgs& a, hipStream_t s) {
@@ -169,15 +174,19 @@ PassArgs base_args(const cgconv_plan* p) {
   return a;
 }
 
-// weights != nullptr: the channel-mixing stage with the unfused passes
+// weights != nullptr: the channel-mixing stage with the unfused passes.
+// scales != nullptr (fp32 only): the adjoint form used by the backward,
+//   out = s_o * conv(s_a * q, s_b * reverse(k)), reverse(k)[n] = k[-n mod N],
+// with per-component scales s_a = scales[0..K), s_b = scales[K..2K),
+// s_o = scales[2K..3K) (device memory), applied in the first and last passes.
 int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf16, hipStream_t s,
-                const float* weights = nullptr) {
+                const float* weights = nullptr, const float* scales = nullptr) {
   const bool mix = weights != nullptr;
   const int K = p->K;
   const long long Wz = (long long)K * p->C;   // complex columns of z
   const long long Ww = (long long)K * p->Cp;  // complex columns of the packed output spectra
-  const int in_pair = bf16 ? IN_PAIR_BF16 : IN_PAIR_F32;
-  const int out_split = bf16 ? OUT_SPLIT_BF16 : OUT_SPLIT_F32;
+  const int in_pair = scales ? IN_PAIR_F32_SCALED_REV : (bf16 ? IN_PAIR_BF16 : IN_PAIR_F32);
+  const int out_split = scales ? OUT_SPLIT_F32_SCALED : (bf16 ? OUT_SPLIT_BF16 : OUT_SPLIT_F32);
   hipError_t e;
   auto pass = [&](int R, int inm, int outm, int dir, int groups, const void* in0, const void* in1, void* o,
                   long long ib, long long ob, int W, int gs_in, int es_in, int gs_out, int fs_out, int inter,
@@ -203,6 +212,10 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     d.a.tw_stride = (int)(p->N / R);
     d.a.inter = inter;
     d.a.scale = scale;
+    if (scales) {
+      d.a.in_scale = scales;
+      d.a.out_scale = scales + 2 * K;
+    }
     return launch_fft_pass(d, s);
   };
   CgArgs ca;
@@ -221,7 +234,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
   const long long N = p->N;
   const float inv_n = 1.0f / (float)N;
   hipEvent_t* ev = nullptr;  // events of this call if it is timed
-  const int kind = mix ? 1 : 0;
+  const int kind = mix ? 1 : (scales ? 2 : 0);  // 2: one half of a backward
   if (p->timing_calls < p->timing_max && (p->timing_kind < 0 || p->timing_kind == kind)) {
     p->timing_kind = kind;
     ev = &p->events[(size_t)p->timing_calls * kMaxEvents];
@@ -463,6 +476,32 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
     }
     p->ws_bytes += (np + nf) * sizeof(float2);
   }
+  {
+    // Backward scales.  The real-basis coefficients obey, path by path,
+    //   R^(J l2 l1)[m1, M, m2] = (-1)^l2 sqrt((2 l1 + 1) / (2 J + 1)) R^(l1 l2 J)[M, m1, m2],
+    // so each gradient is the forward convolution of the output gradient g
+    // with the other operand time-reversed, under per-degree scales:
+    //   dq = s_o * conv(s_a * g, s_b * reverse(k)): s_a = sqrt(2l+1), s_b = (-1)^l, s_o = 1/sqrt(2l+1)
+    //   dk = s_o * conv(s_a * g, reverse(q)):  s_a = (-1)^l sqrt(2l+1), s_b = 1, s_o = (-1)^l/sqrt(2l+1)
+    std::vector<float> bs(6 * (size_t)K);
+    for (int l = 0; l <= L_max; ++l) {
+      const double r = std::sqrt(2.0 * l + 1.0), sg = (l & 1) ? -1.0 : 1.0;
+      for (int c = l * l; c < (l + 1) * (l + 1); ++c) {
+        bs[c] = (float)r;
+        bs[K + c] = (float)sg;
+        bs[2 * K + c] = (float)(1.0 / r);
+        bs[3 * K + c] = (float)(sg * r);
+        bs[4 * K + c] = 1.0f;
+        bs[5 * K + c] = (float)(sg / r);
+      }
+    }
+    if ((e = upload(&p->d_bscale, bs)) != hipSuccess) {
+      set_error("backward scale upload failed: %s", hipGetErrorString(e));
+      (void)hipGetLastError();
+      free_plan(p);
+      return nullptr;
+    }
+  }
   if (L_max <= kMixLmax && C <= kMixCmax) {
     // prepared channel-mixing weights, 2048 bf16 per path
     if ((e = hipMalloc(&p->d_wmix, (size_t)p->paths * 2048 * sizeof(uint16_t))) != hipSuccess) {
@@ -523,7 +562,7 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
     set_error("plan is NULL or ms is NULL");
     return CGCONV_ERR_INVALID_ARG;
   }
-  const int ns = plan->timing_kind == 1 ? plan->n_stages_mix : plan->n_stages;
+  const int ns = plan->timing_kind == 1 ? plan->n_stages_mix : (plan->timing_kind == kKindGate ? 3 : plan->n_stages);
   if (n_stages) *n_stages = ns;
   if (n_calls) *n_calls = plan->timing_calls;
   for (int st = 0; st < cap && st < ns; ++st) ms[st] = 0.0;
@@ -553,6 +592,7 @@ const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
     if (stage >= plan->n_stages_mix) return "";
     return plan->N1 ? kStagesM2[stage] : kStagesM1[stage];
   }
+  if (plan->timing_kind == kKindGate) return stage < 3 ? kStagesG[stage] : "";
   if (stage >= plan->n_stages) return "";
   if (plan->fused) return kStagesF[stage];
   return plan->N1 ? kStages2[stage] : kStages1[stage];
@@ -591,6 +631,47 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
   return run_forward(plan, q, k, out, false, stream, weights);
 }
 
+int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const float* grad_out, float* grad_q,
+                    float* grad_k, hipStream_t stream) {
+  if (!plan) {
+    set_error("plan is NULL");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!q || !k || !grad_out || (!grad_q && !grad_k)) {
+    set_error("q, k and grad_out must be non-NULL, and at least one of grad_q, grad_k");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const void* ptrs[] = {q, k, grad_out, grad_q, grad_k};
+  for (const void* ptr : ptrs) {
+    if (ptr && !aligned16(ptr)) {
+      set_error("q, k, grad_out, grad_q and grad_k must be 16-byte aligned");
+      return CGCONV_ERR_ALIGNMENT;
+    }
+  }
+  for (const float* g : {grad_q, grad_k}) {
+    if (g && (g == q || g == k || g == grad_out)) {
+      set_error("grad_q and grad_k must not alias q, k or grad_out");
+      return CGCONV_ERR_INVALID_ARG;
+    }
+  }
+  if (grad_q && grad_q == grad_k) {
+    set_error("grad_q and grad_k must be distinct");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) {
+    set_error("the plan's device (%d) is not current (%d)", plan->device, cur);
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const int K = plan->K;
+  if (grad_q) {
+    const int st = run_forward(plan, grad_out, k, grad_q, false, stream, nullptr, plan->d_bscale);
+    if (st != CGCONV_OK) return st;
+  }
+  if (grad_k) return run_forward(plan, grad_out, q, grad_k, false, stream, nullptr, plan->d_bscale + 3 * K);
+  return CGCONV_OK;
+}
+
 int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float* f, hipStream_t stream) {
   const int st = check_forward_args(plan, u, v, f);
   if (st != CGCONV_OK) return st;
@@ -603,6 +684,12 @@ int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float*
   a.B = (int)plan->B;
   a.N = (int)plan->N;
   a.C = (int)plan->C;
+  a.events = nullptr;
+  if (plan->timing_calls < plan->timing_max && (plan->timing_kind < 0 || plan->timing_kind == kKindGate)) {
+    plan->timing_kind = kKindGate;
+    a.events = &plan->events[(size_t)plan->timing_calls * kMaxEvents];
+    ++plan->timing_calls;
+  }
   const hipError_t e = launch_gate(plan->L, a, stream);
   if (e != hipSuccess) {
     set_error("kernel launch failed: %s", hipGetErrorString(e));

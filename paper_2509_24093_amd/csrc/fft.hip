@@ -32,6 +32,22 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;                   // round to nearest even
 }
 
+// Per-column input scales of IN_PAIR_F32_SCALED_REV (1 otherwise), read
+// once per column item and applied after all loads of the item are issued.
+struct ColScale {
+  float s0, s1;
+};
+
+template <int INM>
+__device__ __forceinline__ ColScale col_scale(const PassArgs& a, int col) {
+  if constexpr (INM == IN_PAIR_F32_SCALED_REV) {
+    const int kk = col / a.C, K = a.W / a.C;  // W = K * C columns
+    return {a.in_scale[kk], a.in_scale[K + kk]};
+  } else {
+    return {1.f, 1.f};
+  }
+}
+
 template <int INM>
 __device__ __forceinline__ float2 load_elem(const PassArgs& a, int b, long long row, int col) {
   if constexpr (INM == IN_COMPLEX) {
@@ -40,6 +56,11 @@ __device__ __forceinline__ float2 load_elem(const PassArgs& a, int b, long long 
   } else if constexpr (INM == IN_PAIR_F32) {
     const long long i = b * a.in_bstride + row * a.W + col;
     return make_float2(static_cast<const float*>(a.in0)[i], static_cast<const float*>(a.in1)[i]);
+  } else if constexpr (INM == IN_PAIR_F32_SCALED_REV) {
+    const long long base = b * a.in_bstride + col;
+    const long long rrev = (-row) & (long long)a.Nmask;  // -n mod N
+    return make_float2(static_cast<const float*>(a.in0)[base + row * a.W],
+                       static_cast<const float*>(a.in1)[base + rrev * a.W]);
   } else {
     const long long i = b * a.in_bstride + row * a.W + col;
     return make_float2(bf16_to_f32(static_cast<const uint16_t*>(a.in0)[i]),
@@ -62,7 +83,11 @@ __device__ __forceinline__ void store_elem(const PassArgs& a, int b, int g, int 
     const int kk = col / a.Cp, cp = col - kk * a.Cp;
     const long long base = b * a.out_bstride + row * a.KC + (long long)kk * a.C + 2 * cp;
     const bool two = 2 * cp + 1 < a.C;
-    if constexpr (OUTM == OUT_SPLIT_F32) {
+    if constexpr (OUTM == OUT_SPLIT_F32_SCALED) {
+      v.x *= a.out_scale[kk];
+      v.y *= a.out_scale[kk];
+    }
+    if constexpr (OUTM == OUT_SPLIT_F32 || OUTM == OUT_SPLIT_F32_SCALED) {
       float* o = static_cast<float*>(a.out);
       if (two && (a.C % 2 == 0)) {
         *reinterpret_cast<float2*>(o + base) = v;
@@ -115,12 +140,23 @@ __global__ __launch_bounds__(T) void fft_pass_kernel(PassArgs a) {
     const int cl = it % G, j1 = it / G;
     const int col = col0 + cl;
     const bool ok = col < a.W;
+    const ColScale cs = ok ? col_scale<INM>(a, col) : ColScale{0.f, 0.f};
     float2 x[R1];
 #pragma unroll
     for (int t = 0; t < R1; ++t) {
       const int e = j1 + t * (R / R1);
       const long long row = (long long)g * a.gs_in + (long long)e * a.es_in;
       x[t] = ok ? load_elem<INM>(a, b, row, col) : make_float2(0.f, 0.f);
+    }
+    if constexpr (INM == IN_PAIR_F32_SCALED_REV) {
+      // keep the scaling behind the loads (otherwise the loads are issued
+      // in pairs, each waiting for the previous pair's data)
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < R1; ++t) {
+        x[t].x *= cs.s0;
+        x[t].y *= cs.s1;
+      }
     }
     dft_reg<R1, DIR>(x);
     if constexpr (R2 == 1) {
@@ -202,6 +238,9 @@ hipError_t launch_fft_pass(const PassDesc& d, hipStream_t s) {
     switch (d.in_mode) {
       case IN_PAIR_F32: return launch_modes<IN_PAIR_F32, OUT_COMPLEX, -1>(d, s);
       case IN_PAIR_BF16: return launch_modes<IN_PAIR_BF16, OUT_COMPLEX, -1>(d, s);
+      case IN_PAIR_F32_SCALED_REV:
+        if (!d.a.in_scale) return hipErrorInvalidValue;
+        return launch_modes<IN_PAIR_F32_SCALED_REV, OUT_COMPLEX, -1>(d, s);
       case IN_COMPLEX: return launch_modes<IN_COMPLEX, OUT_COMPLEX, -1>(d, s);
       default: return hipErrorInvalidValue;
     }
@@ -211,6 +250,9 @@ hipError_t launch_fft_pass(const PassDesc& d, hipStream_t s) {
     case OUT_COMPLEX: return launch_modes<IN_COMPLEX, OUT_COMPLEX, 1>(d, s);
     case OUT_SPLIT_F32: return launch_modes<IN_COMPLEX, OUT_SPLIT_F32, 1>(d, s);
     case OUT_SPLIT_BF16: return launch_modes<IN_COMPLEX, OUT_SPLIT_BF16, 1>(d, s);
+    case OUT_SPLIT_F32_SCALED:
+      if (!d.a.out_scale) return hipErrorInvalidValue;
+      return launch_modes<IN_COMPLEX, OUT_SPLIT_F32_SCALED, 1>(d, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -40,6 +40,22 @@ __device__ __forceinline__ void degree_norms(const float* x, float (&I)[L + 1]) 
   }
 }
 
+// Online-softmax merge of (maximum, sum of exp(x - maximum)) pairs; a pair
+// with an empty sum is the identity.
+__device__ __forceinline__ void softmax_merge(float& m, float& s, float m2, float s2) {
+  if (s2 == 0.f) return;
+  if (s == 0.f) {
+    m = m2;
+    s = s2;
+    return;
+  }
+  const float nm = fmaxf(m, m2);
+  s = s * __expf(m - nm) + s2 * __expf(m2 - nm);
+  m = nm;
+}
+
+constexpr int kWave = 64;
+
 // Block (chunk, b, channel group): threads = (token slot ts, channel c), c
 // fastest; every thread walks the chunk's tokens ts, ts + TS, ...
 template <int L>
@@ -89,35 +105,36 @@ __global__ __launch_bounds__(kGateThreads) void gate_partials_kernel(const float
       float m = -INFINITY, s = 0.f;
       for (int t = 0; t < TS; ++t) {
         const float2 p = red[t * cpb + tid % cpb][l];
-        if (p.y == 0.f) continue;
-        const float nm = fmaxf(m, p.x);
-        s = s * __expf(m - nm) + p.y * __expf(p.x - nm);
-        m = nm;
+        softmax_merge(m, s, p.x, p.y);
       }
       part[(((long long)b * chunks + chunk) * (L + 1) + l) * C + c] = make_float2(m, s);
     }
   }
 }
 
-// One thread per (b, l, c): combine the chunks' partials.
+// One wave per (b, l, c): each lane merges the partials of chunks lane,
+// lane + 64, ...; the 64 lane results are then merged across the wave.
 template <int L>
 __global__ __launch_bounds__(kGateThreads) void gate_finalize_kernel(const float2* __restrict__ part,
                                                                      float2* __restrict__ fin, int B, int C,
                                                                      int chunks) {
-  const long long t = (long long)blockIdx.x * kGateThreads + threadIdx.x;
-  if (t >= (long long)B * (L + 1) * C) return;
+  const long long t = (long long)blockIdx.x * (kGateThreads / kWave) + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (t >= (long long)B * (L + 1) * C) return;  // whole wave
   const int c = (int)(t % C);
   const int l = (int)((t / C) % (L + 1));
   const long long b = t / ((long long)C * (L + 1));
   float m = -INFINITY, s = 0.f;
-  for (int k = 0; k < chunks; ++k) {
+  for (int k = lane; k < chunks; k += kWave) {
     const float2 p = part[((b * chunks + k) * (L + 1) + l) * C + c];
-    if (p.y == 0.f) continue;
-    const float nm = fmaxf(m, p.x);
-    s = s * __expf(m - nm) + p.y * __expf(p.x - nm);
-    m = nm;
+    softmax_merge(m, s, p.x, p.y);
   }
-  fin[t] = make_float2(m, s);  // [b][l][c]: maximum, denominator
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) {
+    const float m2 = __shfl_xor(m, off, kWave), s2 = __shfl_xor(s, off, kWave);
+    softmax_merge(m, s, m2, s2);
+  }
+  if (lane == 0) fin[t] = make_float2(m, s);  // [b][l][c]: maximum, denominator
 }
 
 // One lane per (b, i, c), c fastest.
@@ -164,18 +181,27 @@ hipError_t launch_gate_value<CGCONV_TU_L>(const GateArgs& a, hipStream_t s) {
   const int chunks = (a.N + kGateChunk - 1) / kGateChunk;
   const int cpb = a.C < kGateThreads ? a.C : kGateThreads;
   const dim3 g1(chunks, a.B, (a.C + cpb - 1) / cpb);
+  auto mark = [&](int i) {
+    if (a.events) (void)hipEventRecord(a.events[i], s);
+  };
+  mark(0);
   hipLaunchKernelGGL(gate_partials_kernel<CGCONV_TU_L>, g1, dim3(kGateThreads), 0, s, a.u, a.part, a.N, a.C,
                      chunks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const long long nf = (long long)a.B * (CGCONV_TU_L + 1) * a.C;
-  hipLaunchKernelGGL(gate_finalize_kernel<CGCONV_TU_L>, dim3((unsigned)((nf + kGateThreads - 1) / kGateThreads)),
-                     dim3(kGateThreads), 0, s, a.part, a.fin, a.B, a.C, chunks);
+  mark(1);
+  const long long nf = (long long)a.B * (CGCONV_TU_L + 1) * a.C;  // one wave each
+  constexpr int wpb = kGateThreads / kWave;
+  hipLaunchKernelGGL(gate_finalize_kernel<CGCONV_TU_L>, dim3((unsigned)((nf + wpb - 1) / wpb)), dim3(kGateThreads), 0,
+                     s, a.part, a.fin, a.B, a.C, chunks);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  mark(2);
   const long long lanes = (long long)a.B * a.N * a.C;
   hipLaunchKernelGGL(gate_value_kernel<CGCONV_TU_L>, dim3((unsigned)((lanes + kGateThreads - 1) / kGateThreads)),
                      dim3(kGateThreads), 0, s, a.u, a.v, a.fin, a.f, a.N, a.C, lanes);
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  mark(3);
+  return hipSuccess;
 }
 
 }  // namespace cgconv

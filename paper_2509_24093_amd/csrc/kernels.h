@@ -11,12 +11,16 @@ namespace cgconv {
 enum InMode : int {
   IN_COMPLEX = 0,   // float2 rows of width W
   IN_PAIR_F32 = 1,  // z = q + i k from two fp32 arrays, rows of width W = K*C
-  IN_PAIR_BF16 = 2  // same, bfloat16 storage
+  IN_PAIR_BF16 = 2, // same, bfloat16 storage
+  // z = s0[k] a[n] + i s1[k] b[-n mod N] (k = column / C): per-component
+  // scales in_scale[0..K) and in_scale[K..2K), second operand time-reversed
+  IN_PAIR_F32_SCALED_REV = 3
 };
 enum OutMode : int {
   OUT_COMPLEX = 0,   // float2 rows of width W
   OUT_SPLIT_F32 = 1, // column (k, cp) -> out[k*C + 2cp] = re, out[k*C + 2cp + 1] = im (if < C)
-  OUT_SPLIT_BF16 = 2 // same, bfloat16 storage (round to nearest even)
+  OUT_SPLIT_BF16 = 2,// same, bfloat16 storage (round to nearest even)
+  OUT_SPLIT_F32_SCALED = 3  // OUT_SPLIT_F32 times out_scale[k]
 };
 
 // One pass of length-R DFTs along the token axis of a [batch][rows][W] array.
@@ -41,6 +45,8 @@ struct PassArgs {
   int Nmask;             // N - 1
   int inter;             // 1: apply the inter-pass twiddle
   float scale;
+  const float* in_scale;  // IN_PAIR_F32_SCALED_REV: [2][K] per-component input scales
+  const float* out_scale; // OUT_SPLIT_F32_SCALED: [K] per-component output scales
 };
 
 struct PassDesc {
@@ -111,6 +117,7 @@ struct GateArgs {
   float2* part;
   float2* fin;
   int B, N, C;
+  hipEvent_t* events;  // optional: 4 events, recorded before, between and after the three kernels
 };
 template <int L>
 hipError_t launch_gate_value(const GateArgs& a, hipStream_t s);

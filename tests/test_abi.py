@@ -129,3 +129,8 @@ def test_mixed_entry_points_reject_bad_arguments():
 def test_gate_entry_point_rejects_null_plan():
     lib = P.library()
     assert lib.cgconv_gate_value(None, 16, 32, 48, None) == P.CGCONV_ERR_INVALID_ARG
+
+
+def test_backward_entry_point_rejects_null_plan():
+    lib = P.library()
+    assert lib.cgconv_backward(None, 16, 32, 48, 64, 80, None) == P.CGCONV_ERR_INVALID_ARG

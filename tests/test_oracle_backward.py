@@ -129,20 +129,18 @@ def test_shared_operand_central_difference():
 
 # ---- planted mistakes -------------------------------------------------------
 
-def _bad_row_direction(Gb, Xb, j, R, wrt_q):
+def _bad_row_direction(GT, XT, j, R, wrt_q):
     """Plant: correlation taken the wrong way round, X[(j - i) mod N]."""
-    N = Gb.shape[0]
-    Xs = Xb[(j - np.arange(N)) % N]
-    P = np.einsum("ioc,iyc->oyc", Gb, Xs)
-    return np.einsum("oxy,oyc->xc", R, P) if wrt_q else np.einsum("oxy,oxc->yc", R, P)
+    N = GT.shape[2]
+    P = np.matmul(GT, XT[:, (j - np.arange(N)) % N, :])
+    return np.tensordot(R, P, axes=([0, 2], [1, 2])) if wrt_q else np.tensordot(R, P, axes=([0, 1], [1, 2]))
 
 
-def _bad_row_transpose(Gb, Xb, j, R, wrt_q):
+def _bad_row_transpose(GT, XT, j, R, wrt_q):
     """Plant: R contracted over the wrong pair of indices (x and y swapped)."""
-    N = Gb.shape[0]
-    Xs = Xb[(np.arange(N) - j) % N]
-    P = np.einsum("ioc,iyc->oyc", Gb, Xs)
-    return np.einsum("oyx,oyc->xc", R, P) if wrt_q else np.einsum("oyx,oxc->yc", R, P)
+    N = GT.shape[2]
+    P = np.matmul(GT, XT[:, (np.arange(N) - j) % N, :])
+    return np.tensordot(R, P, axes=([0, 1], [1, 2])) if wrt_q else np.tensordot(R, P, axes=([0, 2], [1, 2]))
 
 
 @pytest.mark.parametrize("bad", [_bad_row_direction, _bad_row_transpose])
