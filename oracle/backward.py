@@ -39,18 +39,26 @@ def _check(q, k, g, L):
     return q, k, g
 
 
-def _row(Gb, Xb, j, R, wrt_q: bool):
-    """One row of a gradient for one batch element: Gb, Xb (N, K, C) with
-    Xb the other operand; returns (K, C) float64.
+def _prep(Gb, Xb):
+    """Channel-first float64 copies of one batch element: G as [c, o, i] and
+    the other operand X as [c, i, y]."""
+    GT = np.ascontiguousarray(np.transpose(Gb, (2, 1, 0)), dtype=np.float64)
+    XT = np.ascontiguousarray(np.transpose(Xb, (2, 0, 1)), dtype=np.float64)
+    return GT, XT
 
-    P[o, y, c] = sum_i G[i, o, c] X[(i - j) mod N, y, c]; then
-    dq[x] = sum_{o,y} R[o,x,y] P[o,y]  or  dk[y] = sum_{o,x} R[o,x,y] P[o,x]."""
-    N = Gb.shape[0]
-    Xs = Xb[(np.arange(N) - j) % N].astype(np.float64, copy=False)   # X[(i - j) mod N] at i
-    P = np.einsum("ioc,iyc->oyc", Gb.astype(np.float64, copy=False), Xs, optimize=True)
+
+def _row(GT, XT, j, R, wrt_q: bool):
+    """Row j of a gradient for one batch element (GT, XT from _prep, X the
+    other operand); returns (K, C) float64.
+
+    P[c, o, y] = sum_i G[i, o, c] X[(i - j) mod N, y, c] (one matrix product
+    per channel); then dq[x] = sum_{o,y} R[o,x,y] P[o,y] or
+    dk[y] = sum_{o,x} R[o,x,y] P[o,x]."""
+    N = GT.shape[2]
+    P = np.matmul(GT, XT[:, (np.arange(N) - j) % N, :])   # X[(i - j) mod N] at i
     if wrt_q:
-        return np.einsum("oxy,oyc->xc", R, P, optimize=True)
-    return np.einsum("oxy,oxc->yc", R, P, optimize=True)
+        return np.tensordot(R, P, axes=([0, 2], [1, 2]))   # [x, c]
+    return np.tensordot(R, P, axes=([0, 1], [1, 2]))       # [y, c]
 
 
 def backward_direct(q, k, g, L: int):
@@ -61,9 +69,11 @@ def backward_direct(q, k, g, L: int):
     dq = np.empty((B, N, K, C))
     dk = np.empty((B, N, K, C))
     for b in range(B):
+        GT, KT = _prep(g[b], k[b])
+        _, QT = _prep(g[b], q[b])
         for j in range(N):
-            dq[b, j] = _row(g[b], k[b], j, R, True)
-            dk[b, j] = _row(g[b], q[b], j, R, False)
+            dq[b, j] = _row(GT, KT, j, R, True)
+            dk[b, j] = _row(GT, QT, j, R, False)
     return dq, dk
 
 
@@ -73,7 +83,13 @@ def backward_direct_rows(q, k, g, L: int, rows, wrt: str):
     q, k, g = _check(q, k, g, L)
     R = dense_R(L)
     other = k if wrt == "q" else q
-    return np.stack([_row(g[b], other[b], j, R, wrt == "q") for b, j in rows])
+    out = np.empty((len(rows),) + q.shape[2:])
+    for b in sorted({b for b, _ in rows}):   # one batch element at a time
+        GT, XT = _prep(g[b], other[b])
+        for n, (bb, j) in enumerate(rows):
+            if bb == b:
+                out[n] = _row(GT, XT, j, R, wrt == "q")
+    return out
 
 
 def backward_fft(q, k, g, L: int, channels=None):
@@ -86,6 +102,8 @@ def backward_fft(q, k, g, L: int, channels=None):
     q, k, g = (a.astype(np.float64, copy=False) for a in (q, k, g))
     B, N, K, C = q.shape
     R = dense_R(L)
+    Rq = np.transpose(R, (0, 2, 1)).reshape(K * K, K)   # rows (o, y), column x
+    Rk = R.reshape(K * K, K)                            # rows (o, x), column y
     dq = np.empty((B, N, K, C))
     dk = np.empty((B, N, K, C))
     for b in range(B):
@@ -93,8 +111,11 @@ def backward_fft(q, k, g, L: int, channels=None):
             Gh = np.fft.rfft(g[b, :, :, c], axis=0)   # (F, K)
             Qh = np.fft.rfft(q[b, :, :, c], axis=0)
             Kh = np.fft.rfft(k[b, :, :, c], axis=0)
-            dq[b, :, :, c] = np.fft.irfft(np.einsum("oxy,fo,fy->fx", R, Gh, np.conj(Kh), optimize=True),
-                                          n=N, axis=0)
-            dk[b, :, :, c] = np.fft.irfft(np.einsum("oxy,fo,fx->fy", R, Gh, np.conj(Qh), optimize=True),
-                                          n=N, axis=0)
+            F = Gh.shape[0]
+            # dq_hat[f, x] = sum_{o,y} R[o,x,y] G_hat[f,o] conj(k_hat[f,y])
+            Pq = (Gh[:, :, None] * np.conj(Kh)[:, None, :]).reshape(F, K * K)       # (o, y)
+            dq[b, :, :, c] = np.fft.irfft(Pq @ Rq, n=N, axis=0)
+            # dk_hat[f, y] = sum_{o,x} R[o,x,y] G_hat[f,o] conj(q_hat[f,x])
+            Pk = (Gh[:, :, None] * np.conj(Qh)[:, None, :]).reshape(F, K * K)       # (o, x)
+            dk[b, :, :, c] = np.fft.irfft(Pk @ Rk, n=N, axis=0)
     return dq, dk
