@@ -200,7 +200,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: this build runs on one GPU only "
-              "(the path shards over batch and channels with no exchange; see DESIGN.md)", file=sys.stderr)
+              "(the path shards over batch and channels with no exchange between GPUs)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
