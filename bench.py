@@ -199,7 +199,7 @@ def main():
     ap.add_argument("--gate", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: --gpus {args.gpus} is not supported: this build runs on one GPU only "
+        print(f"bench.py: --gpus {args.gpus} is not supported: the benchmark runs on one GPU "
               "(the path shards over batch and channels with no exchange between GPUs)", file=sys.stderr)
         sys.exit(2)
 
