@@ -19,6 +19,9 @@ over the output index and the other operand's index).
 its zeros).  ``backward_fft`` uses the correlation theorem for real signals:
 the DFT over j of sum_i G[i] k[i-j] is G_hat(w) conj(k_hat(w)).
 ``backward_direct_rows`` evaluates the direct sums for selected rows only.
+With ``boundary="linear"`` (the zero-padded token boundary of
+``oracle.conv.cgconv_direct_linear``) the sums keep only the terms whose
+other-operand index i - j lies in 0..N-1.
 Nothing here reuses the GPU path's reading of the backward as a scaled
 forward convolution.  All arithmetic is float64.
 """
@@ -47,7 +50,7 @@ def _prep(Gb, Xb):
     return GT, XT
 
 
-def _row(GT, XT, j, R, wrt_q: bool):
+def _row(GT, XT, j, R, wrt_q: bool, linear: bool = False):
     """Row j of a gradient for one batch element (GT, XT from _prep, X the
     other operand); returns (K, C) float64.
 
@@ -55,13 +58,16 @@ def _row(GT, XT, j, R, wrt_q: bool):
     per channel); then dq[x] = sum_{o,y} R[o,x,y] P[o,y] or
     dk[y] = sum_{o,x} R[o,x,y] P[o,x]."""
     N = GT.shape[2]
-    P = np.matmul(GT, XT[:, (np.arange(N) - j) % N, :])   # X[(i - j) mod N] at i
+    if linear:   # only i >= j: X[i - j] for i = j..N-1
+        P = np.matmul(GT[:, :, j:], XT[:, :N - j, :])
+    else:
+        P = np.matmul(GT, XT[:, (np.arange(N) - j) % N, :])   # X[(i - j) mod N] at i
     if wrt_q:
         return np.tensordot(R, P, axes=([0, 2], [1, 2]))   # [x, c]
     return np.tensordot(R, P, axes=([0, 1], [1, 2]))       # [y, c]
 
 
-def backward_direct(q, k, g, L: int):
+def backward_direct(q, k, g, L: int, boundary: str = "cyclic"):
     """(dq, dk), each (B, N, K, C) float64, from the direct sums."""
     q, k, g = _check(q, k, g, L)
     B, N, K, C = q.shape
@@ -72,12 +78,12 @@ def backward_direct(q, k, g, L: int):
         GT, KT = _prep(g[b], k[b])
         _, QT = _prep(g[b], q[b])
         for j in range(N):
-            dq[b, j] = _row(GT, KT, j, R, True)
-            dk[b, j] = _row(GT, QT, j, R, False)
+            dq[b, j] = _row(GT, KT, j, R, True, boundary == "linear")
+            dk[b, j] = _row(GT, QT, j, R, False, boundary == "linear")
     return dq, dk
 
 
-def backward_direct_rows(q, k, g, L: int, rows, wrt: str):
+def backward_direct_rows(q, k, g, L: int, rows, wrt: str, boundary: str = "cyclic"):
     """Direct sums for selected rows (b, j) of dq (wrt='q') or dk (wrt='k');
     returns (len(rows), K, C) float64."""
     q, k, g = _check(q, k, g, L)
@@ -88,7 +94,7 @@ def backward_direct_rows(q, k, g, L: int, rows, wrt: str):
         GT, XT = _prep(g[b], other[b])
         for n, (bb, j) in enumerate(rows):
             if bb == b:
-                out[n] = _row(GT, XT, j, R, wrt == "q")
+                out[n] = _row(GT, XT, j, R, wrt == "q", boundary == "linear")
     return out
 
 

@@ -9,6 +9,12 @@ every path, as in the path sum after it) with a cyclic token boundary:
 the K x K outer-product accumulator P_i, then a dense contraction with R_full
 (zeros included, so the sparsity logic of the GPU path is not reused).
 
+``cgconv_direct_linear`` and ``cgconv_direct_linear_rows`` give the same
+sum with the zero-padded (linear, causal) token boundary instead: terms with
+i - j < 0 or i - j >= N are absent, so u_i = R_full : sum_{j<=i} q_j (x)
+k_{i-j}.  The paper defines only the token sum (no boundary); this is the
+usual long-convolution boundary, an alternative to the cyclic reading.
+
 ``cgconv_fft`` follows the convolution theorem the paper invokes in §4.1
 (the FFT along the token axis turns the token sum into a pointwise product):
 U_w = R_full : (rfft(q)_w (x) rfft(k)_w), u = irfft(U).  It is exact up to
@@ -114,4 +120,45 @@ def cgconv_fft(q, k, L: int, channels=None, freq_chunk: int = 4096) -> np.ndarra
                 P = Qh[w0:w1, :, None] * Kh[w0:w1, None, :]   # (f, K, K)
                 Uh[w0:w1] = P.reshape(w1 - w0, K * K) @ RK.T
             out[b, :, :, c] = np.fft.irfft(Uh, n=N, axis=0)
+    return out
+
+
+def _rows_direct_linear(qb, kb, i_list, RK):
+    """Linear (zero-padded) token sum for one batch element and a list of
+    output rows: P_i = sum_{j=0}^{i} q_j (x) k_{i-j}; returns
+    (len(i_list), K, C) float64."""
+    N, K, C = qb.shape
+    qT = np.ascontiguousarray(np.transpose(qb, (2, 1, 0)), dtype=np.float64)   # [c, a, j]
+    kT = np.ascontiguousarray(np.transpose(kb, (2, 0, 1)), dtype=np.float64)   # [c, m, b]
+    out = np.empty((len(i_list), K, C))
+    for n, i in enumerate(i_list):
+        js = np.arange(i + 1)
+        P = np.matmul(qT[:, :, js], kT[:, i - js, :])          # sum over j = 0..i
+        out[n] = (P.reshape(C, K * K) @ RK.T).T
+    return out
+
+
+def cgconv_direct_linear(q, k, L: int) -> np.ndarray:
+    """Direct CG convolution with the zero-padded (causal) boundary;
+    returns (B, N, K, C) float64."""
+    q, k = _check(q, k, L)
+    B, N, K, C = q.shape
+    RK = dense_R(L).reshape(K, K * K)
+    out = np.empty((B, N, K, C))
+    for b in range(B):
+        out[b] = _rows_direct_linear(q[b], k[b], list(range(N)), RK)
+    return out
+
+
+def cgconv_direct_linear_rows(q, k, L: int, rows) -> np.ndarray:
+    """Linear-boundary direct mode for selected output rows (b, i)."""
+    q, k = _check(q, k, L, upcast=False)
+    B, N, K, C = q.shape
+    RK = dense_R(L).reshape(K, K * K)
+    out = np.empty((len(rows), K, C))
+    for b in sorted({b for b, _ in rows}):
+        sel = [n for n, (bb, _) in enumerate(rows) if bb == b]
+        res = _rows_direct_linear(q[b], k[b], [rows[n][1] for n in sel], RK)
+        for m, n in enumerate(sel):
+            out[n] = res[m]
     return out

@@ -129,14 +129,14 @@ def test_shared_operand_central_difference():
 
 # ---- planted mistakes -------------------------------------------------------
 
-def _bad_row_direction(GT, XT, j, R, wrt_q):
+def _bad_row_direction(GT, XT, j, R, wrt_q, linear=False):
     """Plant: correlation taken the wrong way round, X[(j - i) mod N]."""
     N = GT.shape[2]
     P = np.matmul(GT, XT[:, (j - np.arange(N)) % N, :])
     return np.tensordot(R, P, axes=([0, 2], [1, 2])) if wrt_q else np.tensordot(R, P, axes=([0, 1], [1, 2]))
 
 
-def _bad_row_transpose(GT, XT, j, R, wrt_q):
+def _bad_row_transpose(GT, XT, j, R, wrt_q, linear=False):
     """Plant: R contracted over the wrong pair of indices (x and y swapped)."""
     N = GT.shape[2]
     P = np.matmul(GT, XT[:, (np.arange(N) - j) % N, :])
