@@ -66,6 +66,31 @@ enum cgconv_status {
  */
 cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_t C);
 
+/* Token boundary of a plan. */
+enum cgconv_boundary {
+  CGCONV_BOUNDARY_CYCLIC = 0, /* k index (i - j) mod N, as cgconv_plan_create */
+  CGCONV_BOUNDARY_LINEAR = 1  /* zero padding: terms with i - j < 0 are absent (causal sum) */
+};
+
+/*
+ * As cgconv_plan_create, with a choice of token boundary.  The paper's
+ * Eq. (EquiConv) gives only the token sum; CGCONV_BOUNDARY_LINEAR reads it
+ * with zero padding, the boundary of causal long convolutions:
+ *
+ *   out[b,i,(J,M),c] = sum_paths sum R^{(l1 l2 J)}[M,m1,m2]
+ *                      * sum_{j=0}^{i} q[b,j,(l1,m1),c] * k[b,i-j,(l2,m2),c]
+ *
+ * computed exactly by DFTs of length Nf = the smallest power of two >= 2N-1
+ * over the zero-padded tokens (no term wraps around).  With the linear
+ * boundary N may be any value 1 <= N <= CGCONV_NMAX/2 (not only a power of
+ * two); q, k, out keep N rows, and the workspace is sized for Nf rows.
+ * Every entry point taking a plan follows its boundary: cgconv_forward,
+ * cgconv_forward_bf16, cgconv_forward_mixed, cgconv_backward (the gradients
+ * of the causal sum) and cgconv_gate_value (softmax over the N tokens).
+ */
+cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N, int32_t L_max, int64_t C,
+                                          int32_t boundary);
+
 /*
  * Enqueue one CG convolution on `stream` (NULL = the legacy default stream),
  * fp32 in, fp32 out, fp32 arithmetic.  Asynchronous: no host synchronisation.

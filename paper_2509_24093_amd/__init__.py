@@ -26,6 +26,8 @@ CGCONV_ERR_OUT_OF_MEMORY = -4
 CGCONV_ERR_HIP = -5
 CGCONV_LMAX = 8
 CGCONV_NMAX = 65536
+CGCONV_BOUNDARY_CYCLIC = 0
+CGCONV_BOUNDARY_LINEAR = 1
 
 _lib = None
 
@@ -48,6 +50,8 @@ def library() -> ctypes.CDLL:
     vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
     lib.cgconv_plan_create.argtypes = [i64, i64, i32, i64]
     lib.cgconv_plan_create.restype = vp
+    lib.cgconv_plan_create_boundary.argtypes = [i64, i64, i32, i64, i32]
+    lib.cgconv_plan_create_boundary.restype = vp
     lib.cgconv_forward.argtypes = [vp, vp, vp, vp, vp]
     lib.cgconv_forward.restype = ctypes.c_int
     lib.cgconv_forward_bf16.argtypes = [vp, vp, vp, vp, vp]
@@ -97,6 +101,13 @@ def _check(status: int) -> int:
 
 def cgconv_plan_create(batch: int, N: int, L_max: int, C: int) -> int:
     h = library().cgconv_plan_create(batch, N, L_max, C)
+    if not h:
+        raise CgconvError(CGCONV_ERR_INVALID_ARG, cgconv_last_error())
+    return h
+
+
+def cgconv_plan_create_boundary(batch: int, N: int, L_max: int, C: int, boundary: int) -> int:
+    h = library().cgconv_plan_create_boundary(batch, N, L_max, C, boundary)
     if not h:
         raise CgconvError(CGCONV_ERR_INVALID_ARG, cgconv_last_error())
     return h
@@ -196,12 +207,17 @@ def cgconv_contract_host(L_max: int, qhat, khat):
 
 class Plan:
     """A plan for q, k, out of shape [batch, N, (L_max+1)^2, C] on the current
-    GPU.  ``plan(q, k)`` returns out; fp32 or bfloat16 tensors."""
+    GPU.  ``plan(q, k)`` returns out; fp32 or bfloat16 tensors.  ``boundary``
+    is "cyclic" (default) or "linear" (zero padding, causal sum)."""
 
-    def __init__(self, batch: int, N: int, L_max: int, C: int):
+    def __init__(self, batch: int, N: int, L_max: int, C: int, boundary: str = "cyclic"):
+        if boundary not in ("cyclic", "linear"):
+            raise ValueError("boundary must be 'cyclic' or 'linear'")
         self.shape = (int(batch), int(N), (int(L_max) + 1) ** 2, int(C))
         self.L_max = int(L_max)
-        self._h = cgconv_plan_create(int(batch), int(N), int(L_max), int(C))
+        self.boundary = boundary
+        code = CGCONV_BOUNDARY_LINEAR if boundary == "linear" else CGCONV_BOUNDARY_CYCLIC
+        self._h = cgconv_plan_create_boundary(int(batch), int(N), int(L_max), int(C), code)
 
     def info(self):
         return cgconv_plan_info(self._h)

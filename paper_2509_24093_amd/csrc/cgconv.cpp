@@ -55,7 +55,9 @@ int ilog2(int64_t x) {
 }  // namespace
 
 struct cgconv_plan {
-  int64_t B = 0, N = 0, C = 0, Cp = 0;
+  int64_t B = 0, N = 0, C = 0, Cp = 0;  // N: length of the token DFTs
+  int64_t Nu = 0;                        // tokens of the caller's arrays (= N, or fewer with zero padding)
+  bool linear = false;                   // zero-padded token boundary
   int L = 0, K = 0;
   int64_t N1 = 0, N2 = 0;  // N1 == 0: single pass
   bool fused = false;      // two-pass with N2 = 64 and the fused middle kernel
@@ -171,6 +173,8 @@ PassArgs base_args(const cgconv_plan* p) {
   a.KC = (int)(p->K * p->C);
   a.Nmask = (int)(p->N - 1);
   a.scale = 1.0f;
+  a.in_rows = (int)p->Nu;
+  a.out_rows = (int)p->Nu;
   return a;
 }
 
@@ -185,7 +189,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
   const int K = p->K;
   const long long Wz = (long long)K * p->C;   // complex columns of z
   const long long Ww = (long long)K * p->Cp;  // complex columns of the packed output spectra
-  const int in_pair = scales ? IN_PAIR_F32_SCALED_REV : (bf16 ? IN_PAIR_BF16 : IN_PAIR_F32);
+  const int in_pair = (scales ? IN_PAIR_F32_SCALED_REV : (bf16 ? IN_PAIR_BF16 : IN_PAIR_F32)) + (p->linear ? 3 : 0);
   const int out_split = scales ? OUT_SPLIT_F32_SCALED : (bf16 ? OUT_SPLIT_BF16 : OUT_SPLIT_F32);
   hipError_t e;
   auto pass = [&](int R, int inm, int outm, int dir, int groups, const void* in0, const void* in1, void* o,
@@ -232,6 +236,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
   ca.n1_log2 = ilog2(p->N1 ? p->N1 : p->N);
   ca.n2_log2 = ilog2(p->N1 ? p->N2 : 1);
   const long long N = p->N;
+  const long long Nu = p->Nu;  // rows of q, k and out (padded rows are implicit zeros)
   const float inv_n = 1.0f / (float)N;
   hipEvent_t* ev = nullptr;  // events of this call if it is timed
   const int kind = mix ? 1 : (scales ? 2 : 0);  // 2: one half of a backward
@@ -253,7 +258,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
   if (p->fused && !mix) {
     // F1 (Y rows w1*64 + n2) -> fused F2 + CG + I1 (V rows w1*64 + n2) -> I2
     const int N1 = (int)p->N1, N2 = 64;
-    e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
+    e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, Nu * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
     if (e != hipSuccess) goto fail;
     mark();
     FusedArgs fa;
@@ -270,12 +275,12 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     e = launch_fused(p->L, fa, s);
     if (e != hipSuccess) goto fail;
     mark();
-    e = pass(N1, IN_COMPLEX, out_split, 1, N2, p->ws2, nullptr, out, N * Ww, N * K * p->C, (int)Ww, 1, N2, 1, N2, 0,
+    e = pass(N1, IN_COMPLEX, out_split, 1, N2, p->ws2, nullptr, out, N * Ww, Nu * K * p->C, (int)Ww, 1, N2, 1, N2, 0,
              inv_n);
     if (e != hipSuccess) goto fail;
     mark();
   } else if (p->N1 == 0) {
-    e = pass((int)N, in_pair, OUT_COMPLEX, -1, 1, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 0, 1, 0, 1, 0, 1.0f);
+    e = pass((int)N, in_pair, OUT_COMPLEX, -1, 1, q, k, p->ws1, Nu * Wz, N * Wz, (int)Wz, 0, 1, 0, 1, 0, 1.0f);
     if (e != hipSuccess) goto fail;
     mark();
     ca.Z = p->ws1;
@@ -284,13 +289,13 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     e = mix ? launch_mix(p->L, ca, s) : launch_cg(p->L, ca, p->force_generic, s);
     if (e != hipSuccess) goto fail;
     mark();
-    e = pass((int)N, IN_COMPLEX, out_split, 1, 1, p->ws2, nullptr, out, N * Ww, N * K * p->C, (int)Ww, 0, 1, 0, 1,
+    e = pass((int)N, IN_COMPLEX, out_split, 1, 1, p->ws2, nullptr, out, N * Ww, Nu * K * p->C, (int)Ww, 0, 1, 0, 1,
              0, inv_n);
     if (e != hipSuccess) goto fail;
     mark();
   } else {
     const int N1 = (int)p->N1, N2 = (int)p->N2;
-    e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, N * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
+    e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, Nu * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
     if (e != hipSuccess) goto fail;
     mark();
     // frequency w1 + N1 w2 goes to row w1 N2 + w2 (contiguous per block, see CgArgs)
@@ -308,7 +313,7 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
              1.0f);
     if (e != hipSuccess) goto fail;
     mark();
-    e = pass(N1, IN_COMPLEX, out_split, 1, N2, p->ws2, nullptr, out, N * Ww, N * K * p->C, (int)Ww, 1, N2, 1, N2, 0,
+    e = pass(N1, IN_COMPLEX, out_split, 1, N2, p->ws2, nullptr, out, N * Ww, Nu * K * p->C, (int)Ww, 1, N2, 1, N2, 0,
              inv_n);
     if (e != hipSuccess) goto fail;
     mark();
@@ -351,17 +356,37 @@ extern "C" {
 const char* cgconv_last_error(void) { return g_last_error.c_str(); }
 
 cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_t C) {
+  return cgconv_plan_create_boundary(batch, N, L_max, C, CGCONV_BOUNDARY_CYCLIC);
+}
+
+cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32_t L_max, int64_t C,
+                                          int32_t boundary) {
   g_last_error.clear();
-  if (batch < 1 || C < 1 || N < 2) {
-    set_error("invalid sizes: batch=%lld N=%lld C=%lld (need batch>=1, N>=2, C>=1)", (long long)batch,
-              (long long)N, (long long)C);
+  if (boundary != CGCONV_BOUNDARY_CYCLIC && boundary != CGCONV_BOUNDARY_LINEAR) {
+    set_error("invalid boundary=%d", boundary);
+    return nullptr;
+  }
+  const bool linear = boundary == CGCONV_BOUNDARY_LINEAR;
+  if (batch < 1 || C < 1 || N_tokens < (linear ? 1 : 2)) {
+    set_error("invalid sizes: batch=%lld N=%lld C=%lld (need batch>=1, N>=%d, C>=1)", (long long)batch,
+              (long long)N_tokens, (long long)C, linear ? 1 : 2);
     return nullptr;
   }
   if (L_max < 0) {
     set_error("invalid L_max=%d", L_max);
     return nullptr;
   }
-  if (!is_pow2(N) || N > CGCONV_NMAX) {
+  // DFT length: N itself (cyclic), or the smallest power of two >= 2N - 1 so
+  // that no term of the zero-padded sum wraps around (linear)
+  int64_t N = N_tokens;
+  if (linear) {
+    if (N_tokens > CGCONV_NMAX / 2) {
+      set_error("unsupported N=%lld: the linear boundary needs N <= %d", (long long)N_tokens, CGCONV_NMAX / 2);
+      return nullptr;
+    }
+    N = 2;
+    while (N < 2 * N_tokens - 1) N *= 2;
+  } else if (!is_pow2(N) || N > CGCONV_NMAX) {
     set_error("unsupported N=%lld: need a power of two <= %d", (long long)N, CGCONV_NMAX);
     return nullptr;
   }
@@ -384,6 +409,8 @@ cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_
   }
   p->B = batch;
   p->N = N;
+  p->Nu = N_tokens;
+  p->linear = linear;
   p->C = C;
   p->Cp = Cp;
   p->L = L_max;
@@ -682,7 +709,7 @@ int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float*
   a.part = plan->d_gpart;
   a.fin = plan->d_gfin;
   a.B = (int)plan->B;
-  a.N = (int)plan->N;
+  a.N = (int)plan->Nu;  // the softmax runs over the caller's tokens
   a.C = (int)plan->C;
   a.events = nullptr;
   if (plan->timing_calls < plan->timing_max && (plan->timing_kind < 0 || plan->timing_kind == kKindGate)) {

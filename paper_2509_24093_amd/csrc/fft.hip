@@ -24,13 +24,18 @@ using dft::dft_reg;
 
 constexpr int kThreads = 256;
 
-__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+// bfloat16 bits held in the low half of a float's bit pattern -> fp32
+__device__ __forceinline__ float widen_bf16(float raw) { return __uint_as_float(__float_as_uint(raw) << 16); }
 
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
   const uint32_t u = __float_as_uint(f);
   if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // quiet NaN
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;                   // round to nearest even
 }
+
+// Padded input modes behave as their unpadded mode for rows < in_rows.
+constexpr bool is_padded(int inm) { return inm >= IN_PAIR_F32_PAD; }
+constexpr int unpadded(int inm) { return is_padded(inm) ? inm - 3 : inm; }
 
 // Per-column input scales of IN_PAIR_F32_SCALED_REV (1 otherwise), read
 // once per column item and applied after all loads of the item are issued.
@@ -40,7 +45,7 @@ struct ColScale {
 
 template <int INM>
 __device__ __forceinline__ ColScale col_scale(const PassArgs& a, int col) {
-  if constexpr (INM == IN_PAIR_F32_SCALED_REV) {
+  if constexpr (unpadded(INM) == IN_PAIR_F32_SCALED_REV) {
     const int kk = col / a.C, K = a.W / a.C;  // W = K * C columns
     return {a.in_scale[kk], a.in_scale[K + kk]};
   } else {
@@ -50,21 +55,31 @@ __device__ __forceinline__ ColScale col_scale(const PassArgs& a, int col) {
 
 template <int INM>
 __device__ __forceinline__ float2 load_elem(const PassArgs& a, int b, long long row, int col) {
-  if constexpr (INM == IN_COMPLEX) {
+  constexpr int M = unpadded(INM);
+  constexpr bool PAD = is_padded(INM);
+  if constexpr (M == IN_COMPLEX) {
     const float2* p = static_cast<const float2*>(a.in0);
     return p[b * a.in_bstride + row * a.W + col];
-  } else if constexpr (INM == IN_PAIR_F32) {
-    const long long i = b * a.in_bstride + row * a.W + col;
-    return make_float2(static_cast<const float*>(a.in0)[i], static_cast<const float*>(a.in1)[i]);
-  } else if constexpr (INM == IN_PAIR_F32_SCALED_REV) {
+  } else if constexpr (M == IN_PAIR_F32_SCALED_REV) {
     const long long base = b * a.in_bstride + col;
     const long long rrev = (-row) & (long long)a.Nmask;  // -n mod N
-    return make_float2(static_cast<const float*>(a.in0)[base + row * a.W],
-                       static_cast<const float*>(a.in1)[base + rrev * a.W]);
+    float2 v = make_float2(0.f, 0.f);
+    if (!PAD || row < a.in_rows) v.x = static_cast<const float*>(a.in0)[base + row * a.W];
+    if (!PAD || rrev < a.in_rows) v.y = static_cast<const float*>(a.in1)[base + rrev * a.W];
+    return v;
   } else {
+    if constexpr (PAD) {
+      if (row >= a.in_rows) return make_float2(0.f, 0.f);
+    }
     const long long i = b * a.in_bstride + row * a.W + col;
-    return make_float2(bf16_to_f32(static_cast<const uint16_t*>(a.in0)[i]),
-                       bf16_to_f32(static_cast<const uint16_t*>(a.in1)[i]));
+    if constexpr (M == IN_PAIR_F32) {
+      return make_float2(static_cast<const float*>(a.in0)[i], static_cast<const float*>(a.in1)[i]);
+    } else {
+      // raw bfloat16 bit patterns; widened to fp32 by widen_bf16 after all
+      // loads of the item are issued
+      return make_float2(__uint_as_float(static_cast<const uint16_t*>(a.in0)[i]),
+                         __uint_as_float(static_cast<const uint16_t*>(a.in1)[i]));
+    }
   }
 }
 
@@ -80,6 +95,7 @@ __device__ __forceinline__ void store_elem(const PassArgs& a, int b, int g, int 
   if constexpr (OUTM == OUT_COMPLEX) {
     static_cast<float2*>(a.out)[b * a.out_bstride + row * a.W + col] = v;
   } else {
+    if (row >= a.out_rows) return;  // rows of the zero padding are not part of the output
     const int kk = col / a.Cp, cp = col - kk * a.Cp;
     const long long base = b * a.out_bstride + row * a.KC + (long long)kk * a.C + 2 * cp;
     const bool two = 2 * cp + 1 < a.C;
@@ -148,15 +164,20 @@ __global__ __launch_bounds__(T) void fft_pass_kernel(PassArgs a) {
       const long long row = (long long)g * a.gs_in + (long long)e * a.es_in;
       x[t] = ok ? load_elem<INM>(a, b, row, col) : make_float2(0.f, 0.f);
     }
-    if constexpr (INM == IN_PAIR_F32_SCALED_REV) {
-      // keep the scaling behind the loads (otherwise the loads are issued
-      // in pairs, each waiting for the previous pair's data)
+    // Keep the scaling and the bf16 widening behind the loads: placed next
+    // to each load (inside its bounds branch), they made every load wait
+    // for the previous one's data.
+    if constexpr (unpadded(INM) == IN_PAIR_F32_SCALED_REV) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int t = 0; t < R1; ++t) {
         x[t].x *= cs.s0;
         x[t].y *= cs.s1;
       }
+    } else if constexpr (unpadded(INM) == IN_PAIR_BF16) {
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < R1; ++t) x[t] = make_float2(widen_bf16(x[t].x), widen_bf16(x[t].y));
     }
     dft_reg<R1, DIR>(x);
     if constexpr (R2 == 1) {
@@ -241,6 +262,11 @@ hipError_t launch_fft_pass(const PassDesc& d, hipStream_t s) {
       case IN_PAIR_F32_SCALED_REV:
         if (!d.a.in_scale) return hipErrorInvalidValue;
         return launch_modes<IN_PAIR_F32_SCALED_REV, OUT_COMPLEX, -1>(d, s);
+      case IN_PAIR_F32_PAD: return launch_modes<IN_PAIR_F32_PAD, OUT_COMPLEX, -1>(d, s);
+      case IN_PAIR_BF16_PAD: return launch_modes<IN_PAIR_BF16_PAD, OUT_COMPLEX, -1>(d, s);
+      case IN_PAIR_F32_SCALED_REV_PAD:
+        if (!d.a.in_scale) return hipErrorInvalidValue;
+        return launch_modes<IN_PAIR_F32_SCALED_REV_PAD, OUT_COMPLEX, -1>(d, s);
       case IN_COMPLEX: return launch_modes<IN_COMPLEX, OUT_COMPLEX, -1>(d, s);
       default: return hipErrorInvalidValue;
     }

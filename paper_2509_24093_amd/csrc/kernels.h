@@ -14,7 +14,12 @@ enum InMode : int {
   IN_PAIR_BF16 = 2, // same, bfloat16 storage
   // z = s0[k] a[n] + i s1[k] b[-n mod N] (k = column / C): per-component
   // scales in_scale[0..K) and in_scale[K..2K), second operand time-reversed
-  IN_PAIR_F32_SCALED_REV = 3
+  IN_PAIR_F32_SCALED_REV = 3,
+  // the three pair modes with zero padding: the input arrays hold in_rows
+  // rows and every row index >= in_rows reads as 0 (mode - 3 = unpadded mode)
+  IN_PAIR_F32_PAD = 4,
+  IN_PAIR_BF16_PAD = 5,
+  IN_PAIR_F32_SCALED_REV_PAD = 6
 };
 enum OutMode : int {
   OUT_COMPLEX = 0,   // float2 rows of width W
@@ -47,6 +52,8 @@ struct PassArgs {
   float scale;
   const float* in_scale;  // IN_PAIR_F32_SCALED_REV: [2][K] per-component input scales
   const float* out_scale; // OUT_SPLIT_F32_SCALED: [K] per-component output scales
+  int in_rows;            // padded pair modes: rows present in the input arrays
+  int out_rows;           // split output modes: rows >= out_rows are not stored
 };
 
 struct PassDesc {

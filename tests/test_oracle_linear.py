@@ -135,3 +135,15 @@ def test_planted_linear_backward_wrap_is_caught(monkeypatch):
     ref = float(np.sum(oc.cgconv_direct_linear(q, k, 1) * g))
     dq, _ = ob.backward_direct(q, k, g, 1, boundary="linear")
     assert abs(np.sum(q * dq) - ref) > 1e-6 * abs(ref)
+
+
+@pytest.mark.parametrize("N,Nf", [(5, 9), (6, 16)])
+def test_linear_backward_equals_padded_cyclic(N, Nf):
+    """The linear gradients are the first N rows of the cyclic gradients of
+    the inputs zero-padded to Nf >= 2N - 1 (the padded output gradient
+    included)."""
+    rng = np.random.default_rng(808 + N)
+    q, k, g = _rand(rng, 2, N, 2, 2)
+    dq, dk = ob.backward_direct(q, k, g, 2, boundary="linear")
+    pq, pk = ob.backward_fft(_pad(q, Nf), _pad(k, Nf), _pad(g, Nf), 2)
+    assert rel_l2(pq[:, :N], dq) < 1e-12 and rel_l2(pk[:, :N], dk) < 1e-12
