@@ -27,7 +27,8 @@ random weights: its own JSON line, the mixing stage against the bf16 matrix
 core peak), --backward (cgconv_backward, both gradients, for a seeded
 output gradient: its own JSON line), --gate (cgconv_gate_value with the
 workload's q and k as u and v: its own JSON line, gate_value against the
-fp32 vector peak).
+fp32 vector peak), --boundary linear (any mode on a plan with the
+zero-padded token boundary: DFTs of length 2N).
 """
 
 from __future__ import annotations
@@ -50,6 +51,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 VALU_PEAK_TFLOPS = 256 * 4 * 32 * 2 * 2.4e9 / 1e12
 METRIC = "CG-conv tokens/sec at N=16384, L_max=6, C=32; achieved HBM GB/s vs peak"
 METRIC_MIXED = "CG-conv with per-path channel mixing, tokens/sec at N=16384, L_max=6, C=32"
+METRIC_LINEAR = "CG-conv with the zero-padded (linear) boundary, tokens/sec at N=16384, L_max=6, C=32"
 METRIC_BACKWARD = "CG-conv backward (grad_q and grad_k), tokens/sec at N=16384, L_max=6, C=32"
 METRIC_GATE = "invariant softmax gating + value tensor product, tokens/sec at N=16384, L_max=6, C=32"
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
@@ -102,11 +104,12 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}), flush=True)
 
 
-def cpu_baseline(q, k, L, budget_s, got):
+def cpu_baseline(q, k, L, budget_s, got, linear=False):
     """Oracle direct mode on sampled output rows; returns the bench object and
     the parity of the GPU output on those rows."""
     import numpy as np
-    from oracle.conv import cgconv_direct_rows
+    from oracle.conv import cgconv_direct_linear_rows, cgconv_direct_rows
+    rows_fn = cgconv_direct_linear_rows if linear else cgconv_direct_rows
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
@@ -127,7 +130,7 @@ def cpu_baseline(q, k, L, budget_s, got):
         if chunk == B - 1:
             picks[0] = N - 1
         part = [(b, i) for i in picks]
-        ref.extend(cgconv_direct_rows(q, k, L, part))
+        ref.extend(rows_fn(q, k, L, part))
         rows.extend(part)
         chunk += 1
         if time.perf_counter() - t0 >= budget_s and chunk >= B:
@@ -145,6 +148,17 @@ def cpu_baseline(q, k, L, budget_s, got):
                      f"(all K components and C channels per row), fp64 numpy, {dt:.1f} s; "
                      f"host exposes {cores} cores"}
     return obj, (num / den) ** 0.5 if den > 0 else 0.0, R
+
+
+def dft_length(N, boundary):
+    """Length of the token DFTs: N (cyclic) or the smallest power of two
+    >= 2N - 1 (zero-padded boundary)."""
+    if boundary == "cyclic":
+        return N
+    n = 2
+    while n < 2 * N - 1:
+        n *= 2
+    return n
 
 
 def cg_roofline(stage_avg, B, N, L, C, n_products, nnz, traffic, traffic_src):
@@ -197,6 +211,7 @@ def main():
     ap.add_argument("--mixed", action="store_true")
     ap.add_argument("--backward", action="store_true")
     ap.add_argument("--gate", action="store_true")
+    ap.add_argument("--boundary", choices=["cyclic", "linear"], default="cyclic")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the benchmark runs on one GPU "
@@ -231,7 +246,7 @@ def main():
         kd = torch.from_numpy(k).cuda()
         esize = 4
     out = torch.empty_like(qd)
-    plan = P.Plan(B, N, L, C)
+    plan = P.Plan(B, N, L, C, boundary=args.boundary)
     if args.mixed:
         bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C)
         return
@@ -260,13 +275,15 @@ def main():
     stage_avg = {s: v / max(ncalls, 1) for s, v in stage_ms.items()}
     tokens = B * N
     S = B * N * K * C * esize                     # one feature tensor in bytes
-    # bytes each kernel must move (inputs read + outputs written), fp32 spectra
-    Sc = B * N * K * C * 4
+    # bytes each kernel must move (inputs read + outputs written), fp32
+    # spectra of the DFT length Nf (N, or 2N with the zero-padded boundary)
+    Nf = dft_length(N, args.boundary)
+    Sc = B * Nf * K * C * 4
     Cp = (C + 1) // 2
-    Sp = B * N * K * Cp * 8
+    Sp = B * Nf * K * Cp * 8
     if "cg_fused" in stage_avg:
         io = {"fft_fwd_1": 2 * S + 2 * Sc, "cg_fused": 2 * Sc + Sp, "fft_inv_2": Sp + S}
-    elif N > 256:
+    elif Nf > 256:
         io = {"fft_fwd_1": 2 * S + 2 * Sc, "fft_fwd_2": 4 * Sc, "cg": 2 * Sc + Sp, "fft_inv_1": 2 * Sp,
               "fft_inv_2": Sp + S}
     else:
@@ -274,11 +291,13 @@ def main():
     stages = {s: {"ms": round(t, 4), "bytes": io.get(s), "gbs": round(io.get(s, 0) / (t * 1e-3) / 1e9, 1)}
               for s, t in stage_avg.items()}
     counters, traffic_src = committed_counters(args.workload) if not args.bf16 else (None, "bf16 run")
-    roofline = cg_roofline(stage_avg, B, N, L, C, n_products, nnz,
+    if args.boundary != "cyclic":
+        counters, traffic_src = None, "counters were taken with the cyclic boundary"
+    roofline = cg_roofline(stage_avg, B, Nf, L, C, n_products, nnz,
                            counters["cg_hbm_bytes_per_launch"] if counters else None, traffic_src)
     hbm_alg_gbs = 3 * S / (ms * 1e-3) / 1e9
     result = {
-        "metric": METRIC,
+        "metric": METRIC if args.boundary == "cyclic" else METRIC_LINEAR,
         "value": tokens / (ms * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -290,7 +309,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16-storage/f32" if args.bf16 else "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C,
+        "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C, "boundary": args.boundary,
                    "parallelism": "single GPU"},
         "hbm": {"algorithmic_bytes_per_step": 3 * S, "achieved_gbs": round(hbm_alg_gbs, 1),
                 "peak_gbs": HBM_PEAK_GBS, "frac": round(hbm_alg_gbs / HBM_PEAK_GBS, 4),
@@ -307,7 +326,7 @@ def main():
         if args.bf16:
             q = W.bf16_bits_to_f32(W.to_bf16_bits(q))
             k = W.bf16_bits_to_f32(W.to_bf16_bits(k))
-        obj, parity, R = cpu_baseline(q, k, L, args.cpu_seconds, got)
+        obj, parity, R = cpu_baseline(q, k, L, args.cpu_seconds, got, linear=args.boundary == "linear")
         result["cpu_baseline"] = obj
         result["parity_rel_l2_sampled_rows"] = parity
         log(f"[bench] parity on {R} rows: rel_l2 = {parity:.3e}")
@@ -360,7 +379,7 @@ def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
         "vs_baseline": None,
         "dtype": "f32 (mixing: bf16 hi/lo split on MFMA, fp32 accumulate)",
         "data": "synthetic",
-        "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C, "paths": n_paths,
+        "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C, "boundary": args.boundary, "paths": n_paths,
                    "weights": "N(0, 1/C), seed 2025", "parallelism": "single GPU"},
         "roofline": {
             "kernel": f"cg_mix_kernel<{L}>",
@@ -380,7 +399,9 @@ def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
         },
         "stages": {s: {"ms": round(t, 4)} for s, t in stage_avg.items()},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.boundary != "cyclic":
+        log("[bench] no CPU baseline for the mixed convolution with the zero-padded boundary")
+    if not args.no_cpu_baseline and args.boundary == "cyclic":
         from oracle.mix import cgconv_mixed_direct_rows
         log(f"[bench] CPU oracle baseline, mixed (~{args.cpu_seconds:.0f} s)")
         got = out.cpu().numpy()
@@ -412,7 +433,7 @@ def _common(args, metric, ms, B, N, L, C, dtype):
     return {"metric": metric, "value": B * N / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": dtype, "data": "synthetic",
-            "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C,
+            "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C, "boundary": args.boundary,
                        "parallelism": "single GPU"}}
 
 
@@ -453,7 +474,9 @@ def bench_backward(args, plan, q, k, qd, kd, B, N, L, C):
     ms, stage_avg = _timed(args, step, plan, calls_per_step=2)
     _, nnz, n_products, _ = plan.info()
     counters, src = committed_counters(args.workload)
-    roofline = cg_roofline(stage_avg, B, N, L, C, n_products, nnz,
+    if args.boundary != "cyclic":
+        counters, src = None, "counters were taken with the cyclic boundary"
+    roofline = cg_roofline(stage_avg, B, dft_length(N, args.boundary), L, C, n_products, nnz,
                            counters["cg_hbm_bytes_per_launch"] if counters else None,
                            (src + "; taken on the forward, same kernel and launch shape") if counters else src)
     result = _common(args, METRIC_BACKWARD, ms, B, N, L, C, "f32")
@@ -470,7 +493,7 @@ def bench_backward(args, plan, q, k, qd, kd, B, N, L, C):
             b = len(rows) % B
             part = [(b, 0 if not rows else int(rng.integers(0, N)))]
             for wrt in ("q", "k"):
-                ref = backward_direct_rows(q, k, g, L, part, wrt)[0]
+                ref = backward_direct_rows(q, k, g, L, part, wrt, boundary=args.boundary)[0]
                 d = got[wrt][part[0]].astype(np.float64) - ref
                 num += float((d * d).sum())
                 den += float((ref * ref).sum())

@@ -151,34 +151,9 @@ __global__ __launch_bounds__(T) void fft_pass_kernel(PassArgs a) {
     if (a.inter) __syncthreads();  // uniform over the block; stage 1 stores use tw_pass
   }
 
-  // stage 1: radix-R1 over inputs e = j1 + t*(R/R1)
-  for (int it = threadIdx.x; it < G * (R / R1); it += T) {
-    const int cl = it % G, j1 = it / G;
-    const int col = col0 + cl;
-    const bool ok = col < a.W;
-    const ColScale cs = ok ? col_scale<INM>(a, col) : ColScale{0.f, 0.f};
-    float2 x[R1];
-#pragma unroll
-    for (int t = 0; t < R1; ++t) {
-      const int e = j1 + t * (R / R1);
-      const long long row = (long long)g * a.gs_in + (long long)e * a.es_in;
-      x[t] = ok ? load_elem<INM>(a, b, row, col) : make_float2(0.f, 0.f);
-    }
-    // Keep the scaling and the bf16 widening behind the loads: placed next
-    // to each load (inside its bounds branch), they made every load wait
-    // for the previous one's data.
-    if constexpr (unpadded(INM) == IN_PAIR_F32_SCALED_REV) {
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int t = 0; t < R1; ++t) {
-        x[t].x *= cs.s0;
-        x[t].y *= cs.s1;
-      }
-    } else if constexpr (unpadded(INM) == IN_PAIR_BF16) {
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int t = 0; t < R1; ++t) x[t] = make_float2(widen_bf16(x[t].x), widen_bf16(x[t].y));
-    }
+  // stage 1: radix-R1 over inputs e = j1 + t*(R/R1); finish_item runs the
+  // DFT of one column item and stores it (to HBM, or to LDS for stage 2)
+  auto finish_item = [&](float2(&x)[R1], int cl, int j1, int col, bool ok) {
     dft_reg<R1, DIR>(x);
     if constexpr (R2 == 1) {
       if (ok) {
@@ -188,6 +163,68 @@ __global__ __launch_bounds__(T) void fft_pass_kernel(PassArgs a) {
     } else {
 #pragma unroll
       for (int t = 0; t < R1; ++t) lds[(j1 * R1 + t) * G + cl] = x[t];
+    }
+  };
+  if (unpadded(INM) == IN_PAIR_BF16 && a.W % 2 == 0 && a.in_bstride % 2 == 0) {
+    // bfloat16 pair input with an even row width: two adjacent columns per
+    // item, one 4-byte load per operand and row (col is even, so every
+    // element index is even and col < W implies col + 1 < W)
+    for (int it = threadIdx.x; it < (G / 2) * (R / R1); it += T) {
+      const int cl = 2 * (it % (G / 2)), j1 = it / (G / 2);
+      const int col = col0 + cl;
+      const bool ok = col < a.W;
+      uint32_t w0[R1], w1[R1];
+#pragma unroll
+      for (int t = 0; t < R1; ++t) {
+        const int e = j1 + t * (R / R1);
+        const long long row = (long long)g * a.gs_in + (long long)e * a.es_in;
+        w0[t] = 0u;
+        w1[t] = 0u;
+        if (ok && (!is_padded(INM) || row < a.in_rows)) {
+          const long long i = b * a.in_bstride + row * a.W + col;
+          w0[t] = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(a.in0) + i);
+          w1[t] = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(a.in1) + i);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);  // widen after all loads are issued
+      float2 x0[R1], x1[R1];
+#pragma unroll
+      for (int t = 0; t < R1; ++t) {
+        x0[t] = make_float2(__uint_as_float(w0[t] << 16), __uint_as_float(w1[t] << 16));
+        x1[t] = make_float2(__uint_as_float(w0[t] & 0xffff0000u), __uint_as_float(w1[t] & 0xffff0000u));
+      }
+      finish_item(x0, cl, j1, col, ok);
+      finish_item(x1, cl + 1, j1, col + 1, ok);
+    }
+  } else {
+    for (int it = threadIdx.x; it < G * (R / R1); it += T) {
+      const int cl = it % G, j1 = it / G;
+      const int col = col0 + cl;
+      const bool ok = col < a.W;
+      const ColScale cs = ok ? col_scale<INM>(a, col) : ColScale{0.f, 0.f};
+      float2 x[R1];
+#pragma unroll
+      for (int t = 0; t < R1; ++t) {
+        const int e = j1 + t * (R / R1);
+        const long long row = (long long)g * a.gs_in + (long long)e * a.es_in;
+        x[t] = ok ? load_elem<INM>(a, b, row, col) : make_float2(0.f, 0.f);
+      }
+      // Keep the scaling and the bf16 widening behind the loads: placed next
+      // to each load (inside its bounds branch), they made every load wait
+      // for the previous one's data.
+      if constexpr (unpadded(INM) == IN_PAIR_F32_SCALED_REV) {
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < R1; ++t) {
+          x[t].x *= cs.s0;
+          x[t].y *= cs.s1;
+        }
+      } else if constexpr (unpadded(INM) == IN_PAIR_BF16) {
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < R1; ++t) x[t] = make_float2(widen_bf16(x[t].x), widen_bf16(x[t].y));
+      }
+      finish_item(x, cl, j1, col, ok);
     }
   }
   if constexpr (R2 > 1) {
