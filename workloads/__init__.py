@@ -21,6 +21,11 @@ available, so these synthetic sets stand in for them):
               1..4 random ellipsoids (semi-axes U[0.2,1]); Y_lm of the surface
               normal times per-channel N(0,1) weights (separate for q and k)
   large       B=2,  N=65536, L=8, C=64  i.i.d. N(0, 1/(2l+1)) per degree
+  graph       B=4,  N=4096,  L=6, C=32  the point-cloud recipe with surface
+              positions kept; features as for pointcloud, plus per sample the
+              eigenbasis U of the normalised Laplacian of the symmetrised
+              16-nearest-neighbour graph of the positions (for the graph
+              Fourier variant of the convolution)
 
 Seeds: workload s uses numpy SeedSequence(s).spawn(3) -> (geometry, q, k)
 streams, s = 1001..1005 in the order above.  Values are generated in float64
@@ -40,6 +45,7 @@ WORKLOADS = {
     "molecule": dict(B=32, N=32, L=4, C=32, seed=1003),
     "pointcloud": dict(B=8, N=16384, L=6, C=32, seed=1004),
     "large": dict(B=2, N=65536, L=8, C=64, seed=1005),
+    "graph": dict(B=4, N=4096, L=6, C=32, seed=1006),
 }
 
 
@@ -204,8 +210,82 @@ def _outer_into(dst, Y, w, rows=1024):
         dst[n0:n0 + rows] = Y[n0:n0 + rows, :, None] * w[None, None, :]
 
 
+def _ellipsoid_points(rg, n, axes, rot, centre):
+    """n points uniform (by area) on an ellipsoid surface; returns (positions,
+    unit normals).  Same rejection rule as _ellipsoid_normals: u uniform on
+    the sphere, accepted with probability proportional to the area element;
+    the point is axes * u, its normal is proportional to u / axes."""
+    a = np.asarray(axes)
+    gmax = 1.0 / a.min()
+    pos, nrm = [], []
+    have = 0
+    while have < n:
+        u = _unit(rg, max(2 * (n - have), 64))
+        g = np.sqrt((u[:, 0] / a[0]) ** 2 + (u[:, 1] / a[1]) ** 2 + (u[:, 2] / a[2]) ** 2)
+        keep = rg.uniform(0.0, gmax, u.shape[0]) < g
+        uk = u[keep]
+        nr = uk / a[None, :]
+        nr /= np.linalg.norm(nr, axis=1, keepdims=True)
+        pos.append(uk * a[None, :])
+        nrm.append(nr)
+        have += uk.shape[0]
+    P = np.concatenate(pos)[:n] @ rot.T + centre
+    Nr = np.concatenate(nrm)[:n] @ rot.T
+    return P, Nr
+
+
+def laplacian_eigenbasis(points, knn: int):
+    """(U, eigenvalues) of the normalised Laplacian I - D^-1/2 A D^-1/2 of the
+    symmetrised knn-nearest-neighbour graph of the points (A_ij = 1 if j is
+    among the knn nearest neighbours of i or i among those of j).  U holds
+    the eigenvectors as columns, eigenvalues ascending (float64)."""
+    P = np.asarray(points, dtype=np.float64)
+    n = P.shape[0]
+    d2 = ((P[:, None, :] - P[None, :, :]) ** 2).sum(-1)
+    np.fill_diagonal(d2, np.inf)
+    nbr = np.argpartition(d2, min(knn, n - 1) - 1, axis=1)[:, :min(knn, n - 1)]
+    A = np.zeros((n, n))
+    A[np.repeat(np.arange(n), nbr.shape[1]), nbr.ravel()] = 1.0
+    A = np.maximum(A, A.T)
+    dinv = 1.0 / np.sqrt(A.sum(1))
+    Lap = np.eye(n) - dinv[:, None] * A * dinv[None, :]
+    lam, U = np.linalg.eigh(Lap)
+    return U, lam
+
+
+def graph_pointcloud(B, N, L, C, seed, knn=16):
+    """Point-cloud features with positions kept and the graph basis: returns
+    q, k (B, N, K, C) float32 and U (B, N, N) float32."""
+    rg, rq, rk = _streams(seed)
+    K = (L + 1) ** 2
+    q = np.empty((B, N, K, C), dtype=np.float32)
+    k = np.empty_like(q)
+    U = np.empty((B, N, N), dtype=np.float32)
+    for b in range(B):
+        n_ell = int(rg.integers(1, 5))
+        axes = rg.uniform(0.2, 1.0, size=(n_ell, 3))
+        rots = [_rotation(rg) for _ in range(n_ell)]
+        centres = rg.uniform(-0.5, 0.5, size=(n_ell, 3))
+        u = _unit(rg, 4096)
+        areas = np.array([4 * pi * np.prod(ax) * np.mean(np.sqrt(((u / ax) ** 2).sum(1)))
+                          for ax in axes])
+        counts = np.floor(N * areas / areas.sum()).astype(int)
+        counts[0] += N - counts.sum()
+        parts = [_ellipsoid_points(rg, int(cnt), axes[e], rots[e], centres[e])
+                 for e, cnt in enumerate(counts) if cnt > 0]
+        order = rg.permutation(N)
+        pos = np.concatenate([p for p, _ in parts])[order]
+        normals = np.concatenate([nr for _, nr in parts])[order]
+        Y = real_ylm(L, normals)
+        _outer_into(q[b], Y, rq.standard_normal(C))
+        _outer_into(k[b], Y, rk.standard_normal(C))
+        U[b] = laplacian_eigenbasis(pos, knn)[0]
+    return q, k, U
+
+
 def make(name: str):
-    """Inputs (q, k) float32 of the named workload."""
+    """Inputs (q, k) float32 of the named workload (for "graph", use
+    graph_pointcloud, which also returns the bases)."""
     w = WORKLOADS[name]
     B, N, L, C, s = w["B"], w["N"], w["L"], w["C"], w["seed"]
     if name == "tiny":
@@ -219,6 +299,9 @@ def make(name: str):
         return pointcloud(B, N, L, C, s)
     if name == "large":
         return iid(B, N, L, C, s, per_degree_variance=True)
+    if name == "graph":
+        q, k, _ = graph_pointcloud(B, N, L, C, s)
+        return q, k
     raise KeyError(name)
 
 
