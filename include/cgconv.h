@@ -53,6 +53,8 @@ enum cgconv_status {
 /* Largest supported degree and token count. */
 #define CGCONV_LMAX 8
 #define CGCONV_NMAX 65536
+/* Largest node count of a graph plan (its bases are N x N per batch element). */
+#define CGCONV_GRAPH_NMAX 16384
 
 /*
  * Create a plan for q, k, out of shape [batch][N][(L_max+1)^2][C].
@@ -130,6 +132,34 @@ int cgconv_forward_bf16(cgconv_plan_t plan, const uint16_t* q, const uint16_t* k
  */
 int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, const float* weights,
                          float* out, hipStream_t stream);
+
+/*
+ * CG convolution in a graph Fourier basis (appendix "Fourier Space
+ * Attention": the eigenvectors U of a graph's normalised Laplacian define the
+ * transform x_hat = U^T x, inverse x = U x_hat, and a spectral convolution
+ * multiplies the transforms frequency by frequency; the result permutes with
+ * the nodes when U does).  With the CG product of §4.1 per graph frequency:
+ *
+ *   q_hat[b,f] = sum_i U[b,i,f] q[b,i],   k_hat[b,f] = sum_i U[b,i,f] k[b,i]
+ *   out[b,i,(J,M),c] = sum_f U[b,i,f] sum_paths sum R^{(l1 l2 J)}[M,m1,m2]
+ *                      * q_hat[b,f,(l1,m1),c] * k_hat[b,f,(l2,m2),c]
+ *
+ * cgconv_plan_create_graph(batch, N, L_max, C): N = nodes per batch element,
+ * 1 <= N <= CGCONV_GRAPH_NMAX (any N); allocates the split operands of the
+ * two transforms (about 16 batch*N^2 + 24 batch*N*K*C bytes).  Such a plan
+ * serves cgconv_forward_graph and cgconv_gate_value only.
+ * cgconv_forward_graph: U DEVICE fp32 [batch][N][N] (row i = node, column f
+ * = graph frequency; orthonormal columns are the caller's responsibility,
+ * the library applies U^T and U as given), q, k, out as for cgconv_forward;
+ * out must not alias U, q or k.  The dense transforms run on the bfloat16
+ * matrix cores with both operands split into high and low parts (relative
+ * error about 2^-16 per product, fp32 accumulation); the per-frequency
+ * product is the generated real-basis contraction.  Same stream and
+ * workspace rules as cgconv_forward.
+ */
+cgconv_plan_t cgconv_plan_create_graph(int64_t batch, int64_t N, int32_t L_max, int64_t C);
+int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, const float* k, float* out,
+                         hipStream_t stream);
 
 /*
  * Backward of cgconv_forward (the models of §5 are trained by gradient
@@ -229,9 +259,10 @@ int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, 
  * cg_fused, fft_inv_2) and the number of timed calls.  The first timed call
  * fixes which kind is timed: plain forwards, mixed forwards (cg_mix replaces
  * cg and the unfused passes are listed), backwards (each of the two
- * gradients is one timed call with the plain stages) or gating calls
- * (gate_partials, gate_finalize, gate_value); calls of the other kinds are
- * not timed.
+ * gradients is one timed call with the plain stages), gating calls
+ * (gate_partials, gate_finalize, gate_value) or graph forwards
+ * (gft_split_u, gft_split_x, gft_gemm_fwd, gft_product, gft_split_uhat,
+ * gft_gemm_inv); calls of the other kinds are not timed.
  * cgconv_plan_stage_name returns a stage's name ("" if out of range).
  */
 int cgconv_plan_enable_timing(cgconv_plan_t plan, int32_t max_calls);

@@ -28,6 +28,7 @@ CGCONV_LMAX = 8
 CGCONV_NMAX = 65536
 CGCONV_BOUNDARY_CYCLIC = 0
 CGCONV_BOUNDARY_LINEAR = 1
+CGCONV_GRAPH_NMAX = 16384
 
 _lib = None
 
@@ -52,6 +53,10 @@ def library() -> ctypes.CDLL:
     lib.cgconv_plan_create.restype = vp
     lib.cgconv_plan_create_boundary.argtypes = [i64, i64, i32, i64, i32]
     lib.cgconv_plan_create_boundary.restype = vp
+    lib.cgconv_plan_create_graph.argtypes = [i64, i64, i32, i64]
+    lib.cgconv_plan_create_graph.restype = vp
+    lib.cgconv_forward_graph.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.cgconv_forward_graph.restype = ctypes.c_int
     lib.cgconv_forward.argtypes = [vp, vp, vp, vp, vp]
     lib.cgconv_forward.restype = ctypes.c_int
     lib.cgconv_forward_bf16.argtypes = [vp, vp, vp, vp, vp]
@@ -111,6 +116,18 @@ def cgconv_plan_create_boundary(batch: int, N: int, L_max: int, C: int, boundary
     if not h:
         raise CgconvError(CGCONV_ERR_INVALID_ARG, cgconv_last_error())
     return h
+
+
+def cgconv_plan_create_graph(batch: int, N: int, L_max: int, C: int) -> int:
+    h = library().cgconv_plan_create_graph(batch, N, L_max, C)
+    if not h:
+        raise CgconvError(CGCONV_ERR_INVALID_ARG, cgconv_last_error())
+    return h
+
+
+def cgconv_forward_graph(plan: int, U: int, q: int, k: int, out: int, stream: int) -> int:
+    """CG convolution in the graph Fourier basis U (device [B][N][N] fp32)."""
+    return _check(library().cgconv_forward_graph(plan, U, q, k, out, stream))
 
 
 def cgconv_forward(plan: int, q: int, k: int, out: int, stream: int) -> int:
@@ -332,3 +349,29 @@ def cgconv(q, k, plan: Plan):
 
         _autograd_fn = _CgconvFn
     return _autograd_fn.apply(q, k, plan)
+
+
+class GraphPlan(Plan):
+    """A graph Fourier plan: ``plan(U, q, k)`` with U [batch, N, N] (columns
+    = graph frequencies) and q, k fp32 [batch, N, (L_max+1)^2, C];
+    ``gate_value`` works as on a token plan."""
+
+    def __init__(self, batch: int, N: int, L_max: int, C: int):
+        self.shape = (int(batch), int(N), (int(L_max) + 1) ** 2, int(C))
+        self.L_max = int(L_max)
+        self.boundary = "graph"
+        self._h = cgconv_plan_create_graph(int(batch), int(N), int(L_max), int(C))
+
+    def forward(self, U, q, k, out=None):
+        import torch
+        if out is None:
+            out = torch.empty(self.shape, dtype=torch.float32, device=q.device)
+        s = self._args(q, k, out, torch.float32)
+        B, N = self.shape[0], self.shape[1]
+        if (not isinstance(U, torch.Tensor) or not U.is_cuda or U.dtype != torch.float32
+                or tuple(U.shape) != (B, N, N) or not U.is_contiguous()):
+            raise ValueError(f"U must be a contiguous float32 GPU tensor of shape {(B, N, N)}")
+        cgconv_forward_graph(self._h, U.data_ptr(), q.data_ptr(), k.data_ptr(), out.data_ptr(), s)
+        return out
+
+    __call__ = forward

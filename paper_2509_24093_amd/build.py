@@ -56,6 +56,7 @@ def build(jobs: int | None = None, verbose: bool = True) -> str:
         ([HIPCC, "-x", "hip", "-c"] + HIP_FLAGS, "cgconv.cpp", "cgconv.o", []),
         ([HIPCC, "-c"] + HIP_FLAGS, "fft.hip", "fft.o", []),
         ([HIPCC, "-c"] + HIP_FLAGS, "cg.hip", "cg.o", []),
+        ([HIPCC, "-c"] + HIP_FLAGS, "gft.hip", "gft.o", []),
     ]
     for L in range(LGEN, -1, -1):  # largest first: it compiles longest
         units.append(([HIPCC, "-c"] + HIP_FLAGS, "cg_gen.hip", "cg_gen_L%d.o" % L,

@@ -58,6 +58,15 @@ struct cgconv_plan {
   int64_t B = 0, N = 0, C = 0, Cp = 0;  // N: length of the token DFTs
   int64_t Nu = 0;                        // tokens of the caller's arrays (= N, or fewer with zero padding)
   bool linear = false;                   // zero-padded token boundary
+  bool graph = false;                    // graph Fourier plan (cgconv_forward_graph only)
+  // graph plans: padded sizes and the split operands of the two transforms
+  int64_t Kp = 0, Mp = 0, KCp = 0;
+  uint16_t *ga_fh = nullptr, *ga_fl = nullptr, *ga_ih = nullptr, *ga_il = nullptr;  // U^T and U, [B][Mp][Kp]
+  uint16_t *gb_fh = nullptr, *gb_fl = nullptr;  // [q | k]^T, [B][2 KCp][Kp]
+  uint16_t *gb_ih = nullptr, *gb_il = nullptr;  // u_hat^T, [B][KCp][Kp]
+  float* g_spec = nullptr;                      // [q_hat | k_hat], [B][n][2 KCp]
+  float* g_uhat = nullptr;                      // [B][n][K C]
+  void* g_block = nullptr;                      // one allocation holding all of the above
   int L = 0, K = 0;
   int64_t N1 = 0, N2 = 0;  // N1 == 0: single pass
   bool fused = false;      // two-pass with N2 = 64 and the fused middle kernel
@@ -99,6 +108,7 @@ void free_plan(cgconv_plan* p) {
   (void)hipFree(p->d_gpart);
   (void)hipFree(p->d_gfin);
   (void)hipFree(p->d_bscale);
+  (void)hipFree(p->g_block);
   for (hipEvent_t ev : p->events) (void)hipEventDestroy(ev);
   (void)hipSetDevice(cur);
   delete p;
@@ -110,9 +120,27 @@ const char* const kStagesF[] = {"fft_fwd_1", "cg_fused", "fft_inv_2"};
 const char* const kStagesM2[] = {"fft_fwd_1", "fft_fwd_2", "cg_mix", "fft_inv_1", "fft_inv_2"};
 const char* const kStagesM1[] = {"fft_fwd", "cg_mix", "fft_inv"};
 const char* const kStagesG[] = {"gate_partials", "gate_finalize", "gate_value"};
-// timing kinds: 0 forward, 1 mixed forward, 2 backward (each gradient one call), 3 gating
+const char* const kStagesGft[] = {"gft_split_u", "gft_split_x", "gft_gemm_fwd", "gft_product", "gft_split_uhat",
+                                  "gft_gemm_inv"};
+// timing kinds: 0 forward, 1 mixed forward, 2 backward (each gradient one call), 3 gating, 4 graph forward
 constexpr int kKindGate = 3;
-constexpr int kMaxEvents = 6;  // stages + 1 of the longest pipeline
+constexpr int kKindGraph = 4;
+constexpr int kMaxEvents = 8;  // stages + 1 of the longest pipeline
+
+hipError_t launch_product(int L, const GftProductArgs& a, hipStream_t s) {
+  switch (L) {
+    case 0: return launch_gft_product<0>(a, s);
+    case 1: return launch_gft_product<1>(a, s);
+    case 2: return launch_gft_product<2>(a, s);
+    case 3: return launch_gft_product<3>(a, s);
+    case 4: return launch_gft_product<4>(a, s);
+    case 5: return launch_gft_product<5>(a, s);
+    case 6: return launch_gft_product<6>(a, s);
+    case 7: return launch_gft_product<7>(a, s);
+    case 8: return launch_gft_product<8>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_gate(int L, const GateArgs& a, hipStream_t s) {
   switch (L) {
@@ -324,7 +352,7 @@ fail:
   return CGCONV_ERR_HIP;
 }
 
-int check_forward_args(cgconv_plan* p, const void* q, const void* k, const void* out) {
+int check_plan_args(cgconv_plan* p, const void* q, const void* k, const void* out) {
   if (!p) {
     set_error("plan is NULL");
     return CGCONV_ERR_INVALID_ARG;
@@ -347,6 +375,29 @@ int check_forward_args(cgconv_plan* p, const void* q, const void* k, const void*
     return CGCONV_ERR_INVALID_ARG;
   }
   return CGCONV_OK;
+}
+
+// gating partials: ceil(Nu / kGateChunk) chunks per batch element
+hipError_t alloc_gate_workspace(cgconv_plan* p) {
+  const size_t chunks = (size_t)((p->Nu + kGateChunk - 1) / kGateChunk);
+  const size_t np = (size_t)p->B * chunks * (p->L + 1) * p->C, nf = (size_t)p->B * (p->L + 1) * p->C;
+  hipError_t e;
+  if ((e = hipMalloc(&p->d_gpart, np * sizeof(float2))) != hipSuccess) return e;
+  if ((e = hipMalloc(&p->d_gfin, nf * sizeof(float2))) != hipSuccess) return e;
+  p->ws_bytes += (np + nf) * sizeof(float2);
+  return hipSuccess;
+}
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// the token-DFT entry points: everything but a graph plan
+int check_forward_args(cgconv_plan* p, const void* q, const void* k, const void* out) {
+  const int st = check_plan_args(p, q, k, out);
+  if (st == CGCONV_OK && p->graph) {
+    set_error("a graph plan takes cgconv_forward_graph (or cgconv_gate_value)");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  return st;
 }
 
 }  // namespace
@@ -490,18 +541,11 @@ cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32
     free_plan(p);
     return nullptr;
   }
-  {
-    // gating partials: ceil(N / kGateChunk) chunks per batch element
-    const size_t chunks = (size_t)((N + kGateChunk - 1) / kGateChunk);
-    const size_t np = (size_t)batch * chunks * (L_max + 1) * C, nf = (size_t)batch * (L_max + 1) * C;
-    if ((e = hipMalloc(&p->d_gpart, np * sizeof(float2))) != hipSuccess ||
-        (e = hipMalloc(&p->d_gfin, nf * sizeof(float2))) != hipSuccess) {
-      set_error("gating workspace allocation failed: %s", hipGetErrorString(e));
-      (void)hipGetLastError();
-      free_plan(p);
-      return nullptr;
-    }
-    p->ws_bytes += (np + nf) * sizeof(float2);
+  if ((e = alloc_gate_workspace(p)) != hipSuccess) {
+    set_error("gating workspace allocation failed: %s", hipGetErrorString(e));
+    (void)hipGetLastError();
+    free_plan(p);
+    return nullptr;
   }
   {
     // Backward scales.  The real-basis coefficients obey, path by path,
@@ -543,6 +587,195 @@ cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32
 }
 
 void cgconv_plan_destroy(cgconv_plan_t plan) { free_plan(plan); }
+
+cgconv_plan_t cgconv_plan_create_graph(int64_t batch, int64_t N, int32_t L_max, int64_t C) {
+  g_last_error.clear();
+  if (batch < 1 || C < 1 || N < 1 || batch > 65535) {
+    set_error("invalid sizes: batch=%lld N=%lld C=%lld (need 1 <= batch <= 65535, N>=1, C>=1)", (long long)batch,
+              (long long)N, (long long)C);
+    return nullptr;
+  }
+  if (L_max < 0 || L_max > CGCONV_LMAX) {
+    set_error("unsupported L_max=%d: 0..%d", L_max, CGCONV_LMAX);
+    return nullptr;
+  }
+  if (N > CGCONV_GRAPH_NMAX) {
+    set_error("unsupported N=%lld: a graph plan holds N x N bases, N <= %d", (long long)N, CGCONV_GRAPH_NMAX);
+    return nullptr;
+  }
+  cgconv_plan* p = new (std::nothrow) cgconv_plan;
+  if (!p) {
+    set_error("host allocation failed");
+    return nullptr;
+  }
+  const int K = (L_max + 1) * (L_max + 1);
+  p->graph = true;
+  p->B = batch;
+  p->N = N;
+  p->Nu = N;
+  p->C = C;
+  p->Cp = (C + 1) / 2;
+  p->L = L_max;
+  p->K = K;
+  p->paths = n_paths(L_max);
+  p->nnz = (int64_t)contraction_terms(L_max).size();
+  p->Kp = round_up(N, 32);
+  p->Mp = round_up(N, 128);
+  p->KCp = round_up((int64_t)K * C, 128);
+  hipError_t e = hipGetDevice(&p->device);
+  if (e != hipSuccess) {
+    set_error("hipGetDevice failed: %s", hipGetErrorString(e));
+    delete p;
+    return nullptr;
+  }
+  // sub-buffers of one allocation, each 256-byte aligned
+  const size_t a_elems = (size_t)batch * p->Mp * p->Kp, bf_elems = (size_t)batch * 2 * p->KCp * p->Kp,
+               bi_elems = (size_t)batch * p->KCp * p->Kp;
+  const size_t spec_elems = (size_t)batch * N * 2 * p->KCp, uhat_elems = (size_t)batch * N * K * C;
+  const size_t sizes[] = {a_elems * 2, a_elems * 2, a_elems * 2, a_elems * 2, bf_elems * 2, bf_elems * 2,
+                          bi_elems * 2, bi_elems * 2, spec_elems * 4, uhat_elems * 4};
+  size_t offs[10], total = 0;
+  for (int i = 0; i < 10; ++i) {
+    offs[i] = total;
+    total += (sizes[i] + 255) / 256 * 256;
+  }
+  if ((e = hipMalloc(&p->g_block, total)) != hipSuccess) {
+    set_error("graph workspace allocation of %zu bytes failed: %s", total, hipGetErrorString(e));
+    (void)hipGetLastError();
+    delete p;
+    return nullptr;
+  }
+  char* base = static_cast<char*>(p->g_block);
+  p->ga_fh = reinterpret_cast<uint16_t*>(base + offs[0]);
+  p->ga_fl = reinterpret_cast<uint16_t*>(base + offs[1]);
+  p->ga_ih = reinterpret_cast<uint16_t*>(base + offs[2]);
+  p->ga_il = reinterpret_cast<uint16_t*>(base + offs[3]);
+  p->gb_fh = reinterpret_cast<uint16_t*>(base + offs[4]);
+  p->gb_fl = reinterpret_cast<uint16_t*>(base + offs[5]);
+  p->gb_ih = reinterpret_cast<uint16_t*>(base + offs[6]);
+  p->gb_il = reinterpret_cast<uint16_t*>(base + offs[7]);
+  p->g_spec = reinterpret_cast<float*>(base + offs[8]);
+  p->g_uhat = reinterpret_cast<float*>(base + offs[9]);
+  p->ws_bytes = total;
+  if ((e = alloc_gate_workspace(p)) != hipSuccess) {
+    set_error("gating workspace allocation failed: %s", hipGetErrorString(e));
+    (void)hipGetLastError();
+    free_plan(p);
+    return nullptr;
+  }
+  return p;
+}
+
+int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, const float* k, float* out,
+                         hipStream_t stream) {
+  const int st = check_plan_args(plan, q, k, out);
+  if (st != CGCONV_OK) return st;
+  if (!plan->graph) {
+    set_error("cgconv_forward_graph needs a plan from cgconv_plan_create_graph");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!U) {
+    set_error("U must be a non-NULL device pointer");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!aligned16(U)) {
+    set_error("U must be 16-byte aligned");
+    return CGCONV_ERR_ALIGNMENT;
+  }
+  if (out == U) {
+    set_error("out must not alias U");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  cgconv_plan* p = plan;
+  hipEvent_t* ev = nullptr;
+  if (p->timing_calls < p->timing_max && (p->timing_kind < 0 || p->timing_kind == kKindGraph)) {
+    p->timing_kind = kKindGraph;
+    ev = &p->events[(size_t)p->timing_calls * kMaxEvents];
+    ++p->timing_calls;
+  }
+  int stage = 0;
+  auto mark = [&]() {
+    if (ev) (void)hipEventRecord(ev[stage], stream);
+    ++stage;
+  };
+  const int B = (int)p->B, n = (int)p->N, KC = p->K * (int)p->C;
+  const int Kp = (int)p->Kp, Mp = (int)p->Mp, KCp = (int)p->KCp;
+  auto split = [&](const float* src, long long src_bs, int ld, int rows, int cols, uint16_t* hi, uint16_t* lo,
+                   long long dst_bs, int dst_rows, bool transpose) {
+    GftSplitArgs a;
+    a.src = src;
+    a.src_bs = src_bs;
+    a.ld = ld;
+    a.src_rows = rows;
+    a.src_cols = cols;
+    a.hi = hi;
+    a.lo = lo;
+    a.dst_bs = dst_bs;
+    a.dst_rows = dst_rows;
+    a.dst_cols = Kp;
+    return launch_gft_split(a, transpose, B, stream);
+  };
+  auto gemm = [&](const uint16_t* ah, const uint16_t* al, const uint16_t* bh, const uint16_t* bl, long long b_bs,
+                  float* c, long long c_bs, int ldc, int N_, int Np) {
+    GftGemmArgs g;
+    g.ah = ah;
+    g.al = al;
+    g.bh = bh;
+    g.bl = bl;
+    g.a_bs = (long long)Mp * Kp;
+    g.b_bs = b_bs;
+    g.c = c;
+    g.c_bs = c_bs;
+    g.ldc = ldc;
+    g.M = n;
+    g.N = N_;
+    g.Kp = Kp;
+    return launch_gft_gemm(g, Mp, Np, B, stream);
+  };
+  const long long nn = (long long)n * n, xbs = (long long)n * KC;
+  hipError_t e;
+  mark();
+  // A operands: U^T (rows = graph frequencies) and U (rows = nodes), k = the other index
+  if ((e = split(U, nn, n, n, n, p->ga_fh, p->ga_fl, (long long)Mp * Kp, Mp, true)) != hipSuccess) goto fail;
+  if ((e = split(U, nn, n, n, n, p->ga_ih, p->ga_il, (long long)Mp * Kp, Mp, false)) != hipSuccess) goto fail;
+  mark();
+  // B operand of the forward transform: [q | k] transposed, q in rows 0..KC-1, k from row KCp
+  if ((e = split(q, xbs, KC, n, KC, p->gb_fh, p->gb_fl, 2LL * KCp * Kp, KCp, true)) != hipSuccess) goto fail;
+  if ((e = split(k, xbs, KC, n, KC, p->gb_fh + (size_t)KCp * Kp, p->gb_fl + (size_t)KCp * Kp, 2LL * KCp * Kp, KCp,
+                 true)) != hipSuccess)
+    goto fail;
+  mark();
+  // [q_hat | k_hat] = U^T [q | k]
+  if ((e = gemm(p->ga_fh, p->ga_fl, p->gb_fh, p->gb_fl, 2LL * KCp * Kp, p->g_spec, (long long)n * 2 * KCp, 2 * KCp,
+                2 * KCp, 2 * KCp)) != hipSuccess)
+    goto fail;
+  mark();
+  {
+    GftProductArgs a;
+    a.spec = p->g_spec;
+    a.spec_bs = (long long)n * 2 * KCp;
+    a.ld = 2 * KCp;
+    a.kb_off = KCp;
+    a.out = p->g_uhat;
+    a.out_bs = xbs;
+    a.B = B;
+    a.n = n;
+    a.C = (int)p->C;
+    if ((e = launch_product(p->L, a, stream)) != hipSuccess) goto fail;
+  }
+  mark();
+  if ((e = split(p->g_uhat, xbs, KC, n, KC, p->gb_ih, p->gb_il, (long long)KCp * Kp, KCp, true)) != hipSuccess)
+    goto fail;
+  mark();
+  // u = U u_hat, written straight into out ([B][n][K][C] = [B][n][KC])
+  if ((e = gemm(p->ga_ih, p->ga_il, p->gb_ih, p->gb_il, (long long)KCp * Kp, out, xbs, KC, KC, KCp)) != hipSuccess)
+    goto fail;
+  mark();
+  return CGCONV_OK;
+fail:
+  set_error("kernel launch failed: %s", hipGetErrorString(e));
+  return CGCONV_ERR_HIP;
+}
 
 int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths_out, int64_t* nnz, int64_t* n_products,
                      size_t* workspace_bytes) {
@@ -589,7 +822,10 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
     set_error("plan is NULL or ms is NULL");
     return CGCONV_ERR_INVALID_ARG;
   }
-  const int ns = plan->timing_kind == 1 ? plan->n_stages_mix : (plan->timing_kind == kKindGate ? 3 : plan->n_stages);
+  const int ns = plan->timing_kind == 1           ? plan->n_stages_mix
+                 : plan->timing_kind == kKindGate  ? 3
+                 : plan->timing_kind == kKindGraph ? 6
+                                                   : plan->n_stages;
   if (n_stages) *n_stages = ns;
   if (n_calls) *n_calls = plan->timing_calls;
   for (int st = 0; st < cap && st < ns; ++st) ms[st] = 0.0;
@@ -620,6 +856,7 @@ const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
     return plan->N1 ? kStagesM2[stage] : kStagesM1[stage];
   }
   if (plan->timing_kind == kKindGate) return stage < 3 ? kStagesG[stage] : "";
+  if (plan->timing_kind == kKindGraph) return stage < 6 ? kStagesGft[stage] : "";
   if (stage >= plan->n_stages) return "";
   if (plan->fused) return kStagesF[stage];
   return plan->N1 ? kStages2[stage] : kStages1[stage];
@@ -664,6 +901,10 @@ int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const fl
     set_error("plan is NULL");
     return CGCONV_ERR_INVALID_ARG;
   }
+  if (plan->graph) {
+    set_error("a graph plan takes cgconv_forward_graph (or cgconv_gate_value)");
+    return CGCONV_ERR_INVALID_ARG;
+  }
   if (!q || !k || !grad_out || (!grad_q && !grad_k)) {
     set_error("q, k and grad_out must be non-NULL, and at least one of grad_q, grad_k");
     return CGCONV_ERR_INVALID_ARG;
@@ -700,7 +941,7 @@ int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const fl
 }
 
 int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float* f, hipStream_t stream) {
-  const int st = check_forward_args(plan, u, v, f);
+  const int st = check_plan_args(plan, u, v, f);
   if (st != CGCONV_OK) return st;
   GateArgs a;
   a.u = u;

@@ -1,5 +1,7 @@
-// Invariant softmax gating and the real-space value tensor product for
-// gfx950 (arXiv 2509.24093, §4.2 Invariant Gating, Algorithm 1 step 5).
+// Token-wise real-basis CG products for gfx950: the invariant softmax gating
+// with the real-space value tensor product (arXiv 2509.24093, §4.2 Invariant
+// Gating, Algorithm 1 step 5), and the product per graph frequency of the
+// graph Fourier variant (appendix "Fourier Space Attention").
 // Built once per L_max (-DCGCONV_TU_L, -DCGCONV_BODY):
 //
 //   I[b,i,l,c] = || u[b,i,(l,.),c] ||_2                     per-degree norm
@@ -173,7 +175,38 @@ __global__ __launch_bounds__(kGateThreads) void gate_value_kernel(const float* _
   for (int k = 0; k < K; ++k) z[(long long)k * C] = out[k];
 }
 
+// One lane per (b, f, c), c fastest: the CG product of the graph transforms.
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gft_product_kernel(GftProductArgs a, long long lanes) {
+  constexpr int K = (L + 1) * (L + 1);
+  const long long p = (long long)blockIdx.x * kGateThreads + threadIdx.x;
+  if (p >= lanes) return;
+  const int c = (int)(p % a.C);
+  const long long bf = p / a.C;  // b * n + f
+  const long long b = bf / a.n, f = bf % a.n;
+  const float* x = a.spec + b * a.spec_bs + f * a.ld + c;
+  float qa[K], ka[K], out[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    qa[k] = x[k * a.C];
+    ka[k] = x[a.kb_off + k * a.C];
+  }
+  CgRealBody<L>::run(qa, ka, out);
+  float* z = a.out + b * a.out_bs + f * (long long)K * a.C + c;
+#pragma unroll
+  for (int k = 0; k < K; ++k) z[k * a.C] = out[k];
+}
+
 }  // namespace
+
+template <>
+hipError_t launch_gft_product<CGCONV_TU_L>(const GftProductArgs& a, hipStream_t s) {
+  if (a.B < 1 || a.n < 1 || a.C < 1 || !a.spec || !a.out) return hipErrorInvalidValue;
+  const long long lanes = (long long)a.B * a.n * a.C;
+  hipLaunchKernelGGL(gft_product_kernel<CGCONV_TU_L>, dim3((unsigned)((lanes + kGateThreads - 1) / kGateThreads)),
+                     dim3(kGateThreads), 0, s, a, lanes);
+  return hipGetLastError();
+}
 
 template <>
 hipError_t launch_gate_value<CGCONV_TU_L>(const GateArgs& a, hipStream_t s) {

@@ -134,3 +134,8 @@ def test_gate_entry_point_rejects_null_plan():
 def test_backward_entry_point_rejects_null_plan():
     lib = P.library()
     assert lib.cgconv_backward(None, 16, 32, 48, 64, 80, None) == P.CGCONV_ERR_INVALID_ARG
+
+
+def test_graph_entry_points_reject_bad_arguments():
+    lib = P.library()
+    assert lib.cgconv_forward_graph(None, 16, 32, 48, 64, None) == P.CGCONV_ERR_INVALID_ARG
