@@ -12,11 +12,10 @@
 // accumulation.
 //
 // gft_split_kernel  fp32 matrix -> zero-padded hi / lo operand arrays in the
-//                   k-contiguous layout the GEMM reads (optionally transposed,
-//                   through a 32 x 32 LDS tile so both sides stay coalesced);
-// gft_gemm_kernel   C[m][n] = sum_k A[m][k] Bt[n][k] with A, Bt stored
-//                   [rows][Kp] (k contiguous): every lane's MFMA fragment is
-//                   one aligned 16-byte load of 8 consecutive k values.
+//                   tiled k-contiguous layout the GEMM reads (optionally
+//                   transposed, through a 32 x 32 LDS tile);
+// gft_gemm_kernel   C[m][n] = sum_k A[m][k] Bt[n][k] with A, Bt in the tiled
+//                   layout, streamed through LDS by direct copies.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -32,9 +31,20 @@ __device__ __forceinline__ uint32_t bf16_rne(float x) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-// dst[o][kk] for o < dst_rows, kk < dst_cols (= Kp), from src[kk][o]
-// (TRANSPOSE) or src[o][kk], zero outside src_rows x src_cols.  Block = 32 x
-// 8 threads over a 32 x 32 tile of dst.
+// Tiled operand layout: an operand X[rows][Kp] (rows a multiple of 128, Kp
+// of 32) is stored as tiles of 128 rows x 32 k, tile (rt, kt) at
+// ((rt * Kp/32 + kt) * 4096) elements, inside a tile [chunk c = k%32 / 8]
+// [row r % 128][k % 8].  A tile is 8 KB of contiguous bf16 (one per hi /
+// lo part), so the GEMM copies it to LDS with fully coalesced 16-byte
+// lanes, and a fragment read (32 rows of one 8-value chunk) is 512
+// contiguous bytes of LDS.
+__device__ __forceinline__ long long tiled_offset(int o, int kk, int Kp) {
+  return ((long long)((o >> 7) * (Kp >> 5) + (kk >> 5)) * 4 + ((kk & 31) >> 3)) * 1024 + (o & 127) * 8 + (kk & 7);
+}
+
+// dst[o][kk] (tiled layout) for o < dst_rows, kk < dst_cols (= Kp), from
+// src[kk][o] (TRANSPOSE) or src[o][kk], zero outside src_rows x src_cols.
+// Block = 32 x 8 threads over a 32 x 32 tile of dst.
 template <bool TRANSPOSE>
 __global__ __launch_bounds__(256) void gft_split_kernel(GftSplitArgs a) {
   __shared__ float tile[32][33];
@@ -42,53 +52,68 @@ __global__ __launch_bounds__(256) void gft_split_kernel(GftSplitArgs a) {
   const int kk0 = blockIdx.x * 32, o0 = blockIdx.y * 32;
   const float* src = a.src + (long long)blockIdx.z * a.src_bs;
   const long long db = (long long)blockIdx.z * a.dst_bs;
-  if (TRANSPOSE) {
-    // read rows kk0.. of src (coalesced along o), write rows o0.. of dst (along kk)
-    for (int y = ty; y < 32; y += 8) {
+  for (int y = ty; y < 32; y += 8) {
+    if (TRANSPOSE) {  // read rows kk0.. of src (coalesced along o)
       const int sr = kk0 + y, sc = o0 + tx;
       tile[y][tx] = (sr < a.src_rows && sc < a.src_cols) ? src[(long long)sr * a.ld + sc] : 0.f;
+    } else {          // read rows o0.. of src (coalesced along kk)
+      const int sr = o0 + y, sc = kk0 + tx;
+      tile[tx][y] = (sr < a.src_rows && sc < a.src_cols) ? src[(long long)sr * a.ld + sc] : 0.f;
     }
-    __syncthreads();
-    for (int y = ty; y < 32; y += 8) {
-      const int o = o0 + y, kk = kk0 + tx;
-      if (o < a.dst_rows && kk < a.dst_cols) {
-        const float x = tile[tx][y];
-        const uint32_t h = bf16_rne(x);
-        a.hi[db + (long long)o * a.dst_cols + kk] = (uint16_t)h;
-        a.lo[db + (long long)o * a.dst_cols + kk] = (uint16_t)bf16_rne(x - __uint_as_float(h << 16));
-      }
-    }
-  } else {
-    for (int y = ty; y < 32; y += 8) {
-      const int o = o0 + y, kk = kk0 + tx;
-      if (o < a.dst_rows && kk < a.dst_cols) {
-        const float x = (o < a.src_rows && kk < a.src_cols) ? src[(long long)o * a.ld + kk] : 0.f;
-        const uint32_t h = bf16_rne(x);
-        a.hi[db + (long long)o * a.dst_cols + kk] = (uint16_t)h;
-        a.lo[db + (long long)o * a.dst_cols + kk] = (uint16_t)bf16_rne(x - __uint_as_float(h << 16));
-      }
+  }
+  __syncthreads();
+  for (int y = ty; y < 32; y += 8) {
+    const int o = o0 + y, kk = kk0 + tx;
+    if (o < a.dst_rows && kk < a.dst_cols) {
+      const float x = tile[tx][y];  // element (o, kk)
+      const uint32_t h = bf16_rne(x);
+      const long long off = db + tiled_offset(o, kk, a.dst_cols);
+      a.hi[off] = (uint16_t)h;
+      a.lo[off] = (uint16_t)bf16_rne(x - __uint_as_float(h << 16));
     }
   }
 }
 
 constexpr int kTile = 128;  // block tile (rows and columns of C)
+constexpr int kStageBytes = 4 * 8192;  // A hi, A lo, B hi, B lo tiles of one 32-deep slice
 
-// Block (tile n, tile m, batch) computes a 128 x 128 tile of C with 4 waves
-// of 64 x 64 (2 x 2 MFMA tiles of 32 x 32).  Lane l of a fragment holds row
-// (or column) l % 32 and k values 8 (l / 32) .. +7 of the 16-deep step; the
-// result register r of lane l is row 8 (r / 4) + 4 (l / 32) + r % 4, column
-// l % 32 of the 32 x 32 tile.
-__global__ __launch_bounds__(256) void gft_gemm_kernel(GftGemmArgs g) {
-  const int b = blockIdx.z;
+// Block computes a 128 x 128 tile of C with 4 waves of 64 x 64 (2 x 2 MFMA
+// tiles of 32 x 32).  The 32-deep slices of its A and B row tiles stream
+// through two LDS buffers (32 KB each): the copy of slice kt + 1 (one
+// global_load_lds per wave and KB) is in flight while slice kt is used.
+// Lane l of a fragment holds row (or column) l % 32 and k values
+// 8 (l / 32) .. +7 of a 16-deep step; result register r of lane l is row
+// 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32 of the 32 x 32 tile.
+// Tiles are taken in bands of 4 row tiles, each XCD a contiguous run of the
+// band order, so the blocks in flight on one XCD share their A and B slices
+// in its L2.
+__global__ __launch_bounds__(256, 2) void gft_gemm_kernel(GftGemmArgs g, int Mt, int Nt, int per_xcd) {
+  __shared__ __attribute__((aligned(16))) char lds[2 * kStageBytes];
+  const int b = blockIdx.y;
+  const int id = blockIdx.x;
+  const int t = (id & 7) * per_xcd + (id >> 3);  // tile index in band order
+  if (t >= Mt * Nt) return;                      // whole block
+  const int band = t / (4 * Nt), r4 = t % (4 * Nt);
+  const int bh = min(4, Mt - 4 * band);
+  const int tm = 4 * band + r4 % bh, tn = r4 / bh;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m0 = blockIdx.y * kTile + (wave >> 1) * 64, n0 = blockIdx.x * kTile + (wave & 1) * 64;
-  const int fr = lane & 31, fk = (lane >> 5) * 8;
-  const long long Kp = g.Kp;
-  const uint16_t* ah = g.ah + b * g.a_bs + (long long)(m0 + fr) * Kp + fk;
-  const uint16_t* al = g.al + b * g.a_bs + (long long)(m0 + fr) * Kp + fk;
-  const uint16_t* bh = g.bh + b * g.b_bs + (long long)(n0 + fr) * Kp + fk;
-  const uint16_t* bl = g.bl + b * g.b_bs + (long long)(n0 + fr) * Kp + fk;
-  const long long step32 = 32 * Kp;  // second row (column) tile of the wave
+  const int wm = wave >> 1, wn = wave & 1;
+  const int KT = g.Kp >> 5;
+  // this block's A and B row tiles (8 KB per 32-deep slice, slices contiguous)
+  const uint16_t* srcs[4] = {g.ah + b * g.a_bs + (long long)tm * kTile * g.Kp,
+                             g.al + b * g.a_bs + (long long)tm * kTile * g.Kp,
+                             g.bh + b * g.b_bs + (long long)tn * kTile * g.Kp,
+                             g.bl + b * g.b_bs + (long long)tn * kTile * g.Kp};
+  auto copy_slice = [&](int kt, int buf) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int ch = wave + 4 * i;  // KB chunk of the 32 KB stage: part ch / 8, KB ch % 8
+      const uint16_t* src = srcs[ch >> 3] + (long long)kt * 4096 + (ch & 7) * 512 + lane * 8;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(lds + buf * kStageBytes + ch * 1024),
+                                       16, 0, 0);
+    }
+  };
 
   v16f acc[2][2];
 #pragma unroll
@@ -98,31 +123,42 @@ __global__ __launch_bounds__(256) void gft_gemm_kernel(GftGemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  auto load = [&](v8bf (&f)[8], long long k) {
-    f[0] = *reinterpret_cast<const v8bf*>(ah + k);
-    f[1] = *reinterpret_cast<const v8bf*>(ah + step32 + k);
-    f[2] = *reinterpret_cast<const v8bf*>(al + k);
-    f[3] = *reinterpret_cast<const v8bf*>(al + step32 + k);
-    f[4] = *reinterpret_cast<const v8bf*>(bh + k);
-    f[5] = *reinterpret_cast<const v8bf*>(bh + step32 + k);
-    f[6] = *reinterpret_cast<const v8bf*>(bl + k);
-    f[7] = *reinterpret_cast<const v8bf*>(bl + step32 + k);
-  };
-  v8bf cur[8], nxt[8];
-  load(cur, 0);
-  for (long long k = 0; k < Kp; k += 16) {
-    if (k + 16 < Kp) load(nxt, k + 16);  // next step's fragments in flight during this step
+  const int fr = lane & 31, fc = lane >> 5;
+  copy_slice(0, 0);
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) {
+      copy_slice(kt + 1, buf ^ 1);
+      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // this wave's copies of slice kt have landed
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    __syncthreads();  // every wave's copies of slice kt are visible
+    const char* st = lds + buf * kStageBytes;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int s = 0; s < 2; ++s) {
+      const int c = 2 * s + fc;  // k chunk of this lane's 8 values
+      v8bf a_h[2], a_l[2], b_h[2], b_l[2];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur[i], cur[4 + j], acc[i][j], 0, 0, 0);
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur[i], cur[6 + j], acc[i][j], 0, 0, 0);
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur[2 + i], cur[4 + j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < 2; ++i) {
+        const int ra = wm * 64 + 32 * i + fr, rb = wn * 64 + 32 * i + fr;
+        a_h[i] = *reinterpret_cast<const v8bf*>(st + 0 * 8192 + (c * 128 + ra) * 16);
+        a_l[i] = *reinterpret_cast<const v8bf*>(st + 1 * 8192 + (c * 128 + ra) * 16);
+        b_h[i] = *reinterpret_cast<const v8bf*>(st + 2 * 8192 + (c * 128 + rb) * 16);
+        b_l[i] = *reinterpret_cast<const v8bf*>(st + 3 * 8192 + (c * 128 + rb) * 16);
       }
 #pragma unroll
-    for (int x = 0; x < 8; ++x) cur[x] = nxt[x];
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_h[i], b_h[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_h[i], b_l[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_l[i], b_h[j], acc[i][j], 0, 0, 0);
+        }
+    }
+    __syncthreads();  // slice kt is consumed before its buffer is refilled
   }
+  const int m0 = tm * kTile + wm * 64, n0 = tn * kTile + wn * 64;
   float* c = g.c + b * g.c_bs;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -150,10 +186,12 @@ hipError_t launch_gft_split(const GftSplitArgs& a, bool transpose, int batch, hi
 }
 
 hipError_t launch_gft_gemm(const GftGemmArgs& g, int Mp, int Np, int batch, hipStream_t s) {
-  // operands hold Mp (Np) rows of Kp values: whole tiles and 16-deep steps
-  if (Mp % kTile || Np % kTile || g.Kp % 16 || g.Kp <= 0 || g.M > Mp || g.N > Np || batch <= 0)
+  // operands hold Mp (Np) rows of Kp values in the tiled layout: whole tiles
+  if (Mp % kTile || Np % kTile || g.Kp % 32 || g.Kp <= 0 || g.M > Mp || g.N > Np || batch <= 0)
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gft_gemm_kernel, dim3(Np / kTile, Mp / kTile, batch), dim3(256), 0, s, g);
+  const int Mt = Mp / kTile, Nt = Np / kTile;
+  const int per_xcd = (Mt * Nt + 7) / 8;
+  hipLaunchKernelGGL(gft_gemm_kernel, dim3(8 * per_xcd, batch), dim3(256), 0, s, g, Mt, Nt, per_xcd);
   return hipGetLastError();
 }
 
