@@ -27,7 +27,9 @@ random weights: its own JSON line, the mixing stage against the bf16 matrix
 core peak), --backward (cgconv_backward, both gradients, for a seeded
 output gradient: its own JSON line), --gate (cgconv_gate_value with the
 workload's q and k as u and v: its own JSON line, gate_value against the
-fp32 vector peak), --boundary linear (any mode on a plan with the
+fp32 vector peak), --graph (cgconv_forward_graph on the graph workload,
+B=4, N=4096, L=6, C=32, with Laplacian eigenbases: its own JSON line, the
+forward transform against the bf16 matrix core peak), --boundary linear (any mode on a plan with the
 zero-padded token boundary: DFTs of length 2N).
 """
 
@@ -51,6 +53,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 VALU_PEAK_TFLOPS = 256 * 4 * 32 * 2 * 2.4e9 / 1e12
 METRIC = "CG-conv tokens/sec at N=16384, L_max=6, C=32; achieved HBM GB/s vs peak"
 METRIC_MIXED = "CG-conv with per-path channel mixing, tokens/sec at N=16384, L_max=6, C=32"
+METRIC_GRAPH = "CG-conv in a graph Fourier basis, tokens/sec at N=4096, L_max=6, C=32"
 METRIC_LINEAR = "CG-conv with the zero-padded (linear) boundary, tokens/sec at N=16384, L_max=6, C=32"
 METRIC_BACKWARD = "CG-conv backward (grad_q and grad_k), tokens/sec at N=16384, L_max=6, C=32"
 METRIC_GATE = "invariant softmax gating + value tensor product, tokens/sec at N=16384, L_max=6, C=32"
@@ -212,6 +215,7 @@ def main():
     ap.add_argument("--backward", action="store_true")
     ap.add_argument("--gate", action="store_true")
     ap.add_argument("--boundary", choices=["cyclic", "linear"], default="cyclic")
+    ap.add_argument("--graph", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the benchmark runs on one GPU "
@@ -232,6 +236,9 @@ def main():
         copy_calibration()
         return
 
+    if args.graph:
+        bench_graph(args)
+        return
     w = W.WORKLOADS[args.workload]
     B, N, L, C = w["B"], w["N"], w["L"], w["C"]
     K = (L + 1) ** 2
@@ -566,6 +573,78 @@ def bench_gate(args, plan, q, k, qd, kd, out, B, N, L, C):
                                             f"({tokens:.0f} token-equivalents), fp64 numpy, {dt:.1f} s"}
         result["parity_rel_l2_sampled_channels"] = (num / den) ** 0.5
         log(f"[bench] gating parity on {len(chans)} channels: rel_l2 = {result['parity_rel_l2_sampled_channels']:.3e}")
+    else:
+        result["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(result), flush=True)
+
+
+def bench_graph(args):
+    """cgconv_forward_graph on the graph workload: per sample the normalised
+    Laplacian eigenbasis of the 16-nearest-neighbour graph of its points."""
+    import numpy as np
+    import torch
+
+    import paper_2509_24093_amd as P
+    import workloads as W
+    w = W.WORKLOADS["graph"]
+    B, N, L, C = w["B"], w["N"], w["L"], w["C"]
+    log(f"[bench] generating the graph workload B={B} N={N} L={L} C={C} (Laplacian eigenbases on the host)")
+    q, k, U = W.graph_pointcloud(B, N, L, C, w["seed"])
+    qd, kd, Ud = (torch.from_numpy(a).cuda() for a in (q, k, U))
+    plan = P.GraphPlan(B, N, L, C)
+    out = torch.empty_like(qd)
+    log(f"[bench] timing {args.steps} graph steps")
+    ms, stage_avg = _timed(args, lambda: plan(Ud, qd, kd, out), plan)
+    K = (L + 1) ** 2
+    Kp = -(-N // 32) * 32
+    Mp = -(-N // 128) * 128
+    KCp = -(-(K * C) // 128) * 128
+    mfma_flops = 3 * 2 * Mp * (2 * KCp) * Kp * B       # executed bf16 MFMA work of the forward transform
+    fp32_equiv = 2 * N * N * (2 * K * C) * B             # the transform itself
+    gm = stage_avg["gft_gemm_fwd"]
+    achieved = mfma_flops / (gm * 1e-3) / 1e12
+    result = _common(args, METRIC_GRAPH, ms, B, N, L, C, "f32 (transforms: bf16 hi/lo split on MFMA, fp32 accumulate)")
+    result["config"] = {"workload": "graph", "batch": B, "N": N, "L_max": L, "C": C,
+                        "basis": "normalised Laplacian eigenvectors of the 16-NN graph", "parallelism": "single GPU"}
+    result["roofline"] = {
+        "kernel": "gft_gemm_kernel (forward transform)",
+        "bound": "mfma",
+        "achieved": round(achieved, 2),
+        "peak": MFMA_BF16_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+        "traffic": None,
+        "flops_per_launch": mfma_flops,
+        "flop_model": (f"bf16 MFMA flops executed: 3 products (hi*hi, hi*lo, lo*hi) x 2 x Mp={Mp} x Np={2 * KCp} "
+                       f"x Kp={Kp} per batch element, {B} elements; the transform itself is "
+                       f"2*N^2*2KC*B = {fp32_equiv} fp32 flops"),
+        "transform_tflops_fp32_equivalent": round(fp32_equiv / (gm * 1e-3) / 1e12, 2),
+        "launch_ms": round(gm, 4),
+    }
+    result["stages"] = {s: {"ms": round(t, 4)} for s, t in stage_avg.items()}
+    if not args.no_cpu_baseline:
+        from oracle.gft import gft_cgconv
+        log(f"[bench] CPU oracle baseline, graph (~{args.cpu_seconds:.0f} s)")
+        got = out.cpu().numpy()
+        num = den = 0.0
+        chans = []
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_seconds and len(chans) < C:
+            c = len(chans)
+            ref = gft_cgconv(U[0:1], q[0:1, :, :, c:c + 1], k[0:1, :, :, c:c + 1], L)
+            d = got[0:1, :, :, c:c + 1].astype(np.float64) - ref
+            num += float((d * d).sum())
+            den += float((ref * ref).sum())
+            chans.append(c)
+        dt = time.perf_counter() - t0
+        tokens = N * len(chans) / C
+        result["cpu_baseline"] = {"value": tokens / dt, "unit": "tokens/s", "cores": len(os.sched_getaffinity(0)),
+                                  "kind": "oracle",
+                                  "sample": f"batch element 0, all {N} nodes, channels 0..{len(chans) - 1} of {C} "
+                                            f"({tokens:.0f} token-equivalents), fp64 numpy, {dt:.1f} s"}
+        result["parity_rel_l2_sampled_channels"] = (num / den) ** 0.5
+        log(f"[bench] graph parity on {len(chans)} channels: rel_l2 = {result['parity_rel_l2_sampled_channels']:.3e}")
     else:
         result["cpu_baseline"] = None
     plan.close()
