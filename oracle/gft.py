@@ -39,3 +39,23 @@ def gft_cgconv(U, q, k, L: int) -> np.ndarray:
     kh = np.einsum("bif,biyc->bfyc", U, k, optimize=True)    # U^T k
     uh = np.einsum("oxy,bfxc,bfyc->bfoc", dense_R(L), qh, kh, optimize=True)
     return np.einsum("bif,bfoc->bioc", U, uh, optimize=True)  # U u_hat
+
+
+def gft_backward(U, q, k, G, L: int):
+    """(dq, dk) of a scalar loss with dL/du = G, by the chain rule through the
+    three steps: G_hat = U^T G (the adjoint of the inverse transform u = U
+    u_hat), dL/dq_hat[f,x] = sum_{o,y} R_full[o,x,y] G_hat[f,o] k_hat[f,y]
+    (and likewise for k_hat), then dq = U dL/dq_hat (the adjoint of q_hat =
+    U^T q).  float64."""
+    U = np.asarray(U, dtype=np.float64)
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    G = np.asarray(G, dtype=np.float64)
+    R = dense_R(L)
+    qh = np.einsum("bif,bixc->bfxc", U, q, optimize=True)
+    kh = np.einsum("bif,biyc->bfyc", U, k, optimize=True)
+    Gh = np.einsum("bif,bioc->bfoc", U, G, optimize=True)
+    dqh = np.einsum("oxy,bfoc,bfyc->bfxc", R, Gh, kh, optimize=True)
+    dkh = np.einsum("oxy,bfoc,bfxc->bfyc", R, Gh, qh, optimize=True)
+    return (np.einsum("bif,bfxc->bixc", U, dqh, optimize=True),
+            np.einsum("bif,bfyc->biyc", U, dkh, optimize=True))

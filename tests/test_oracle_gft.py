@@ -143,3 +143,43 @@ def test_planted_transform_mistakes(monkeypatch):
         return real_einsum(spec, *ops, **kw)
     monkeypatch.setattr(og.np, "einsum", bad_inverse)
     assert rel_l2(og.gft_cgconv(U, q, k, L), good) > 1e-3
+
+
+@pytest.mark.parametrize("n,L", [(1, 2), (5, 2), (7, 3)])
+def test_backward_adjoint_identity(n, L):
+    """<u(q, k), G> = <q, dq> = <k, dk> (u is bilinear), against the pinned
+    forward; with an orthonormal and with a general (non-orthogonal) basis,
+    since the chain rule does not need orthogonality."""
+    rng = np.random.default_rng(910 + n)
+    q, k = _rand(rng, 2, n, L, 2)
+    G = rng.normal(size=q.shape)
+    for U in (_orth(rng, 2, n), rng.normal(size=(2, n, n))):
+        ref = float(np.sum(og.gft_cgconv(U, q, k, L) * G))
+        dq, dk = og.gft_backward(U, q, k, G, L)
+        assert abs(np.sum(q * dq) - ref) <= 1e-11 * abs(ref)
+        assert abs(np.sum(k * dk) - ref) <= 1e-11 * abs(ref)
+
+
+def test_backward_unit_tensors_and_autograd():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(911)
+    B, n, L, C = 1, 3, 1, 2
+    U = _orth(rng, B, n)
+    q, k = _rand(rng, B, n, L, C)
+    G = rng.normal(size=q.shape)
+    dq, dk = og.gft_backward(U, q, k, G, L)
+    for j in range(n):
+        for x in range((L + 1) ** 2):
+            e = np.zeros_like(q)
+            e[0, j, x, 1] = 1.0
+            assert dq[0, j, x, 1] == pytest.approx(np.sum(og.gft_cgconv(U, e, k, L) * G), abs=1e-12)
+            assert dk[0, j, x, 1] == pytest.approx(np.sum(og.gft_cgconv(U, q, e, L) * G), abs=1e-12)
+    from oracle.cg import dense_R
+    tU, tR = torch.from_numpy(U), torch.from_numpy(dense_R(L))
+    tq = torch.tensor(q, requires_grad=True)
+    tk = torch.tensor(k, requires_grad=True)
+    qh = torch.einsum("bif,bixc->bfxc", tU, tq)
+    kh = torch.einsum("bif,biyc->bfyc", tU, tk)
+    u = torch.einsum("bif,bfoc->bioc", tU, torch.einsum("oxy,bfxc,bfyc->bfoc", tR, qh, kh))
+    (u * torch.from_numpy(G)).sum().backward()
+    assert rel_l2(tq.grad.numpy(), dq) < 1e-13 and rel_l2(tk.grad.numpy(), dk) < 1e-13
