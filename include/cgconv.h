@@ -147,7 +147,8 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
  * cgconv_plan_create_graph(batch, N, L_max, C): N = nodes per batch element,
  * 1 <= N <= CGCONV_GRAPH_NMAX (any N); allocates the split operands of the
  * two transforms (about 16 batch*N^2 + 24 batch*N*K*C bytes).  Such a plan
- * serves cgconv_forward_graph and cgconv_gate_value only.
+ * serves cgconv_forward_graph, cgconv_backward_graph and cgconv_gate_value
+ * only.
  * cgconv_forward_graph: U DEVICE fp32 [batch][N][N] (row i = node, column f
  * = graph frequency; orthonormal columns are the caller's responsibility,
  * the library applies U^T and U as given), q, k, out as for cgconv_forward;
@@ -160,6 +161,17 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
 cgconv_plan_t cgconv_plan_create_graph(int64_t batch, int64_t N, int32_t L_max, int64_t C);
 int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, const float* k, float* out,
                          hipStream_t stream);
+/*
+ * Backward of cgconv_forward_graph: given grad_out = dL/dout, the gradients
+ * with respect to q and k (the chain rule through U^T, the per-frequency
+ * product and U; valid for any U).  As for cgconv_backward, each gradient
+ * is one forward pipeline of the same kernels with per-degree scales on the
+ * per-frequency product (the transposition identity of the real-basis
+ * tensor); the bases are split once for both.  Arguments and aliasing rules
+ * as cgconv_backward, plus U as for cgconv_forward_graph.
+ */
+int cgconv_backward_graph(cgconv_plan_t plan, const float* U, const float* q, const float* k,
+                          const float* grad_out, float* grad_q, float* grad_k, hipStream_t stream);
 
 /*
  * Backward of cgconv_forward (the models of §5 are trained by gradient

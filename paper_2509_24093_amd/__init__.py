@@ -57,6 +57,8 @@ def library() -> ctypes.CDLL:
     lib.cgconv_plan_create_graph.restype = vp
     lib.cgconv_forward_graph.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.cgconv_forward_graph.restype = ctypes.c_int
+    lib.cgconv_backward_graph.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.cgconv_backward_graph.restype = ctypes.c_int
     lib.cgconv_forward.argtypes = [vp, vp, vp, vp, vp]
     lib.cgconv_forward.restype = ctypes.c_int
     lib.cgconv_forward_bf16.argtypes = [vp, vp, vp, vp, vp]
@@ -128,6 +130,11 @@ def cgconv_plan_create_graph(batch: int, N: int, L_max: int, C: int) -> int:
 def cgconv_forward_graph(plan: int, U: int, q: int, k: int, out: int, stream: int) -> int:
     """CG convolution in the graph Fourier basis U (device [B][N][N] fp32)."""
     return _check(library().cgconv_forward_graph(plan, U, q, k, out, stream))
+
+
+def cgconv_backward_graph(plan: int, U: int, q: int, k: int, grad_out: int, grad_q, grad_k, stream: int) -> int:
+    """Gradients of the graph Fourier convolution (grad_q or grad_k may be None)."""
+    return _check(library().cgconv_backward_graph(plan, U, q, k, grad_out, grad_q, grad_k, stream))
 
 
 def cgconv_forward(plan: int, q: int, k: int, out: int, stream: int) -> int:
@@ -373,5 +380,21 @@ class GraphPlan(Plan):
             raise ValueError(f"U must be a contiguous float32 GPU tensor of shape {(B, N, N)}")
         cgconv_forward_graph(self._h, U.data_ptr(), q.data_ptr(), k.data_ptr(), out.data_ptr(), s)
         return out
+
+    def backward(self, U, q, k, grad_out, need_q: bool = True, need_k: bool = True):
+        """(grad_q, grad_k) given grad_out (fp32); an unneeded one is None."""
+        import torch
+        if not (need_q or need_k):
+            return None, None
+        s = self._args(q, k, grad_out, torch.float32)
+        B, N = self.shape[0], self.shape[1]
+        if (not isinstance(U, torch.Tensor) or not U.is_cuda or U.dtype != torch.float32
+                or tuple(U.shape) != (B, N, N) or not U.is_contiguous()):
+            raise ValueError(f"U must be a contiguous float32 GPU tensor of shape {(B, N, N)}")
+        gq = torch.empty(self.shape, dtype=torch.float32, device=q.device) if need_q else None
+        gk = torch.empty(self.shape, dtype=torch.float32, device=q.device) if need_k else None
+        cgconv_backward_graph(self._h, U.data_ptr(), q.data_ptr(), k.data_ptr(), grad_out.data_ptr(),
+                              gq.data_ptr() if gq is not None else None, gk.data_ptr() if gk is not None else None, s)
+        return gq, gk
 
     __call__ = forward

@@ -377,6 +377,31 @@ int check_plan_args(cgconv_plan* p, const void* q, const void* k, const void* ou
   return CGCONV_OK;
 }
 
+// Backward scales.  The real-basis coefficients obey, path by path,
+//   R^(J l2 l1)[m1, M, m2] = (-1)^l2 sqrt((2 l1 + 1) / (2 J + 1)) R^(l1 l2 J)[M, m1, m2],
+// so each gradient is the forward convolution of the output gradient g
+// with the other operand time-reversed (token DFT) or as is (graph basis),
+// under per-degree scales:
+//   dq = s_o * conv(s_a * g, s_b * k'):  s_a = sqrt(2l+1), s_b = (-1)^l, s_o = 1/sqrt(2l+1)
+//   dk = s_o * conv(s_a * g, q'):        s_a = (-1)^l sqrt(2l+1), s_b = 1, s_o = (-1)^l/sqrt(2l+1)
+// Table [dq: s_a, s_b, s_o][dk: s_a, s_b, s_o], K floats each.
+hipError_t upload_backward_scales(cgconv_plan* p) {
+  const int K = p->K;
+  std::vector<float> bs(6 * (size_t)K);
+  for (int l = 0; l <= p->L; ++l) {
+    const double r = std::sqrt(2.0 * l + 1.0), sg = (l & 1) ? -1.0 : 1.0;
+    for (int c = l * l; c < (l + 1) * (l + 1); ++c) {
+      bs[c] = (float)r;
+      bs[K + c] = (float)sg;
+      bs[2 * K + c] = (float)(1.0 / r);
+      bs[3 * K + c] = (float)(sg * r);
+      bs[4 * K + c] = 1.0f;
+      bs[5 * K + c] = (float)(sg / r);
+    }
+  }
+  return upload(&p->d_bscale, bs);
+}
+
 // gating partials: ceil(Nu / kGateChunk) chunks per batch element
 hipError_t alloc_gate_workspace(cgconv_plan* p) {
   const size_t chunks = (size_t)((p->Nu + kGateChunk - 1) / kGateChunk);
@@ -547,31 +572,11 @@ cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32
     free_plan(p);
     return nullptr;
   }
-  {
-    // Backward scales.  The real-basis coefficients obey, path by path,
-    //   R^(J l2 l1)[m1, M, m2] = (-1)^l2 sqrt((2 l1 + 1) / (2 J + 1)) R^(l1 l2 J)[M, m1, m2],
-    // so each gradient is the forward convolution of the output gradient g
-    // with the other operand time-reversed, under per-degree scales:
-    //   dq = s_o * conv(s_a * g, s_b * reverse(k)): s_a = sqrt(2l+1), s_b = (-1)^l, s_o = 1/sqrt(2l+1)
-    //   dk = s_o * conv(s_a * g, reverse(q)):  s_a = (-1)^l sqrt(2l+1), s_b = 1, s_o = (-1)^l/sqrt(2l+1)
-    std::vector<float> bs(6 * (size_t)K);
-    for (int l = 0; l <= L_max; ++l) {
-      const double r = std::sqrt(2.0 * l + 1.0), sg = (l & 1) ? -1.0 : 1.0;
-      for (int c = l * l; c < (l + 1) * (l + 1); ++c) {
-        bs[c] = (float)r;
-        bs[K + c] = (float)sg;
-        bs[2 * K + c] = (float)(1.0 / r);
-        bs[3 * K + c] = (float)(sg * r);
-        bs[4 * K + c] = 1.0f;
-        bs[5 * K + c] = (float)(sg / r);
-      }
-    }
-    if ((e = upload(&p->d_bscale, bs)) != hipSuccess) {
-      set_error("backward scale upload failed: %s", hipGetErrorString(e));
-      (void)hipGetLastError();
-      free_plan(p);
-      return nullptr;
-    }
+  if ((e = upload_backward_scales(p)) != hipSuccess) {
+    set_error("backward scale upload failed: %s", hipGetErrorString(e));
+    (void)hipGetLastError();
+    free_plan(p);
+    return nullptr;
   }
   if (L_max <= kMixLmax && C <= kMixCmax) {
     // prepared channel-mixing weights, 2048 bf16 per path
@@ -657,8 +662,8 @@ cgconv_plan_t cgconv_plan_create_graph(int64_t batch, int64_t N, int32_t L_max, 
   p->g_spec = reinterpret_cast<float*>(base + offs[8]);
   p->g_uhat = reinterpret_cast<float*>(base + offs[9]);
   p->ws_bytes = total;
-  if ((e = alloc_gate_workspace(p)) != hipSuccess) {
-    set_error("gating workspace allocation failed: %s", hipGetErrorString(e));
+  if ((e = alloc_gate_workspace(p)) != hipSuccess || (e = upload_backward_scales(p)) != hipSuccess) {
+    set_error("graph plan set-up failed: %s", hipGetErrorString(e));
     (void)hipGetLastError();
     free_plan(p);
     return nullptr;
@@ -666,27 +671,15 @@ cgconv_plan_t cgconv_plan_create_graph(int64_t batch, int64_t N, int32_t L_max, 
   return p;
 }
 
-int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, const float* k, float* out,
-                         hipStream_t stream) {
-  const int st = check_plan_args(plan, q, k, out);
-  if (st != CGCONV_OK) return st;
-  if (!plan->graph) {
-    set_error("cgconv_forward_graph needs a plan from cgconv_plan_create_graph");
-    return CGCONV_ERR_INVALID_ARG;
-  }
-  if (!U) {
-    set_error("U must be a non-NULL device pointer");
-    return CGCONV_ERR_INVALID_ARG;
-  }
-  if (!aligned16(U)) {
-    set_error("U must be 16-byte aligned");
-    return CGCONV_ERR_ALIGNMENT;
-  }
-  if (out == U) {
-    set_error("out must not alias U");
-    return CGCONV_ERR_INVALID_ARG;
-  }
-  cgconv_plan* p = plan;
+}  // extern "C"
+
+namespace {
+
+// One graph pipeline: out = U R:((U^T x1) (x) (U^T x2)), with per-component
+// scales of the product when `scales` is set; split_u = false reuses the
+// split bases of the previous pipeline on this plan.
+int run_graph(cgconv_plan* p, const float* U, const float* x1, const float* x2, float* out, const float* scales,
+              bool split_u, hipStream_t stream) {
   hipEvent_t* ev = nullptr;
   if (p->timing_calls < p->timing_max && (p->timing_kind < 0 || p->timing_kind == kKindGraph)) {
     p->timing_kind = kKindGraph;
@@ -736,12 +729,14 @@ int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, con
   hipError_t e;
   mark();
   // A operands: U^T (rows = graph frequencies) and U (rows = nodes), k = the other index
-  if ((e = split(U, nn, n, n, n, p->ga_fh, p->ga_fl, (long long)Mp * Kp, Mp, true)) != hipSuccess) goto fail;
-  if ((e = split(U, nn, n, n, n, p->ga_ih, p->ga_il, (long long)Mp * Kp, Mp, false)) != hipSuccess) goto fail;
+  if (split_u) {
+    if ((e = split(U, nn, n, n, n, p->ga_fh, p->ga_fl, (long long)Mp * Kp, Mp, true)) != hipSuccess) goto fail;
+    if ((e = split(U, nn, n, n, n, p->ga_ih, p->ga_il, (long long)Mp * Kp, Mp, false)) != hipSuccess) goto fail;
+  }
   mark();
   // B operand of the forward transform: [q | k] transposed, q in rows 0..KC-1, k from row KCp
-  if ((e = split(q, xbs, KC, n, KC, p->gb_fh, p->gb_fl, 2LL * KCp * Kp, KCp, true)) != hipSuccess) goto fail;
-  if ((e = split(k, xbs, KC, n, KC, p->gb_fh + (size_t)KCp * Kp, p->gb_fl + (size_t)KCp * Kp, 2LL * KCp * Kp, KCp,
+  if ((e = split(x1, xbs, KC, n, KC, p->gb_fh, p->gb_fl, 2LL * KCp * Kp, KCp, true)) != hipSuccess) goto fail;
+  if ((e = split(x2, xbs, KC, n, KC, p->gb_fh + (size_t)KCp * Kp, p->gb_fl + (size_t)KCp * Kp, 2LL * KCp * Kp, KCp,
                  true)) != hipSuccess)
     goto fail;
   mark();
@@ -761,6 +756,7 @@ int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, con
     a.B = B;
     a.n = n;
     a.C = (int)p->C;
+    a.scales = scales;
     if ((e = launch_product(p->L, a, stream)) != hipSuccess) goto fail;
   }
   mark();
@@ -775,6 +771,76 @@ int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, con
 fail:
   set_error("kernel launch failed: %s", hipGetErrorString(e));
   return CGCONV_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cgconv_forward_graph(cgconv_plan_t plan, const float* U, const float* q, const float* k, float* out,
+                         hipStream_t stream) {
+  const int st = check_plan_args(plan, q, k, out);
+  if (st != CGCONV_OK) return st;
+  if (!plan->graph) {
+    set_error("cgconv_forward_graph needs a plan from cgconv_plan_create_graph");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!U) {
+    set_error("U must be a non-NULL device pointer");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!aligned16(U)) {
+    set_error("U must be 16-byte aligned");
+    return CGCONV_ERR_ALIGNMENT;
+  }
+  if (out == U) {
+    set_error("out must not alias U");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  return run_graph(plan, U, q, k, out, nullptr, true, stream);
+}
+
+int cgconv_backward_graph(cgconv_plan_t plan, const float* U, const float* q, const float* k, const float* grad_out,
+                          float* grad_q, float* grad_k, hipStream_t stream) {
+  if (!plan || !plan->graph) {
+    set_error("cgconv_backward_graph needs a plan from cgconv_plan_create_graph");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!U || !q || !k || !grad_out || (!grad_q && !grad_k)) {
+    set_error("U, q, k and grad_out must be non-NULL, and at least one of grad_q, grad_k");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const void* ptrs[] = {U, q, k, grad_out, grad_q, grad_k};
+  for (const void* ptr : ptrs) {
+    if (ptr && !aligned16(ptr)) {
+      set_error("U, q, k, grad_out, grad_q and grad_k must be 16-byte aligned");
+      return CGCONV_ERR_ALIGNMENT;
+    }
+  }
+  for (const float* g : {grad_q, grad_k}) {
+    if (g && (g == U || g == q || g == k || g == grad_out)) {
+      set_error("grad_q and grad_k must not alias U, q, k or grad_out");
+      return CGCONV_ERR_INVALID_ARG;
+    }
+  }
+  if (grad_q && grad_q == grad_k) {
+    set_error("grad_q and grad_k must be distinct");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) {
+    set_error("the plan's device (%d) is not current (%d)", plan->device, cur);
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const int K = plan->K;
+  bool split_u = true;
+  if (grad_q) {
+    const int st = run_graph(plan, U, grad_out, k, grad_q, plan->d_bscale, true, stream);
+    if (st != CGCONV_OK) return st;
+    split_u = false;
+  }
+  if (grad_k) return run_graph(plan, U, grad_out, q, grad_k, plan->d_bscale + 3 * K, split_u, stream);
+  return CGCONV_OK;
 }
 
 int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths_out, int64_t* nnz, int64_t* n_products,

@@ -191,7 +191,18 @@ __global__ __launch_bounds__(kGateThreads) void gft_product_kernel(GftProductArg
     qa[k] = x[k * a.C];
     ka[k] = x[a.kb_off + k * a.C];
   }
+  if (a.scales) {  // uniform
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      qa[k] *= a.scales[k];
+      ka[k] *= a.scales[K + k];
+    }
+  }
   CgRealBody<L>::run(qa, ka, out);
+  if (a.scales) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) out[k] *= a.scales[2 * K + k];
+  }
   float* z = a.out + b * a.out_bs + f * (long long)K * a.C + c;
 #pragma unroll
   for (int k = 0; k < K; ++k) z[k * a.C] = out[k];

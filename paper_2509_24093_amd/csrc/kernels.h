@@ -162,6 +162,7 @@ struct GftProductArgs {
   float* out;
   long long out_bs;
   int B, n, C;
+  const float* scales;  // optional [3][K]: q_hat, k_hat and u_hat per component (backward)
 };
 template <int L>
 hipError_t launch_gft_product(const GftProductArgs& a, hipStream_t s);

@@ -139,3 +139,4 @@ def test_backward_entry_point_rejects_null_plan():
 def test_graph_entry_points_reject_bad_arguments():
     lib = P.library()
     assert lib.cgconv_forward_graph(None, 16, 32, 48, 64, None) == P.CGCONV_ERR_INVALID_ARG
+    assert lib.cgconv_backward_graph(None, 16, 32, 48, 64, 80, 96, None) == P.CGCONV_ERR_INVALID_ARG

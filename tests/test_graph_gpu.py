@@ -8,7 +8,8 @@ Gaussian matrices) for node counts that are and are not multiples of the
 128-row tiles, L_max 0..8, odd C and C = 1; a normalised Laplacian
 eigenbasis with the node-permutation property checked on the GPU output;
 the graph workload at full size (B=4, N=4096, L=6, C=32) on a channel
-subset (channels are independent); gating on a graph plan; argument errors.
+subset (channels are independent); the backward (orthonormal and general
+bases, a skipped gradient); gating on a graph plan; argument errors.
 """
 
 import numpy as np
@@ -16,7 +17,7 @@ import pytest
 
 import workloads as W
 from oracle.gate import gate_value
-from oracle.gft import gft_cgconv
+from oracle.gft import gft_backward, gft_cgconv
 from tests.conftest import rel_l2
 
 pytestmark = pytest.mark.gpu
@@ -132,3 +133,27 @@ def test_graph_argument_errors():
     torch.cuda.synchronize()
     g.close()
     t.close()
+
+
+@pytest.mark.parametrize("shape,orth", [((1, 5, 2, 2), True), ((2, 130, 3, 3), True), ((1, 300, 6, 2), True),
+                                        ((1, 64, 4, 3), False)], ids=["B1N5", "B2N130", "B1N300L6", "general"])
+def test_graph_backward(shape, orth):
+    torch = _torch()
+    import paper_2509_24093_amd as P
+    B, n, L, C = shape
+    rng = np.random.default_rng(6400 + n)
+    U = _orth(rng, B, n) if orth else (rng.normal(size=(B, n, n)) / np.sqrt(n)).astype(np.float32)
+    q, k = W.iid(B, n, L, C, seed=6401 + n)
+    g = rng.normal(size=q.shape).astype(np.float32)
+    print(f"[gpu] cgconv_backward_graph B={B} N={n} L={L} C={C} orthonormal={orth}", flush=True)
+    plan = P.GraphPlan(B, n, L, C)
+    dev = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in (U, q, k, g)]
+    gq, gk = plan.backward(*dev)
+    _, gk2 = plan.backward(*dev, need_q=False)
+    torch.cuda.synchronize()
+    gq, gk, gk2 = gq.cpu().numpy(), gk.cpu().numpy(), gk2.cpu().numpy()
+    plan.close()
+    rq, rk = gft_backward(U, q, k, g, L)
+    eq, ek = rel_l2(gq, rq), rel_l2(gk, rk)
+    print(f"[parity] graph backward {shape} orthonormal={orth}: dq {eq:.3e} dk {ek:.3e}", flush=True)
+    assert eq <= TOL and ek <= TOL and rel_l2(gk2, rk) <= TOL
