@@ -160,14 +160,19 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
   const int pp = w1 == 0 ? ((kN2 - p) & (kN2 - 1)) : (kN2 - 1 - p);
   const int C = a.C;
 
-  for (int x = tid; x < kN2; x += kThreadsF) {
-    const int t = x >> 3, j = x & 7;
-    sTw8[x] = a.tw[(long long)(j * t) * (N / kN2)];
+  // twiddles: loaded first, written to LDS once the first chunks' loads are
+  // issued (the load counter is in order: waiting for these then waits for
+  // nothing younger)
+  static_assert(2 * kN2 <= kThreadsF, "one twiddle per thread");
+  float2 tw8v = make_float2(0.f, 0.f), twpv = make_float2(0.f, 0.f);
+  if (tid < kN2) {
+    const int t = tid >> 3, j = tid & 7;
+    tw8v = a.tw[(long long)(j * t) * (N / kN2)];
   }
-  for (int x = tid; x < 2 * kN2; x += kThreadsF) {
-    const int cls = x / kN2, n2 = x % kN2;
+  if (tid < 2 * kN2) {
+    const int cls = tid / kN2, n2 = tid % kN2;
     const long long e = ((long long)n2 * (cls ? w1b : w1)) & (N - 1);
-    sTwp[x] = conjf2(a.tw[e]);
+    twpv = a.tw[e];  // conjugated when written (no use of the value before then)
   }
 
   float2 qa[K], ka[K];
@@ -230,21 +235,31 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
     for (int s2 = 0; s2 < 8; ++s2) d[8 * s2 * KC * kCc] = x[s2];
   };
   const int j2_0 = tid / NCOL, j2_1 = (tid + kThreadsF) / NCOL;
-  // All chunks' HBM loads are issued up front (as many loads in flight as
-  // the unfused kernel has): every chunk consumed frees 32 raw registers and
-  // fills 28 input registers, so the peak is the raw data itself.
+  // HBM loads run kLookahead chunks ahead of stage 1, in chunk order (kept by
+  // scheduling barriers): chunk q's stage 1 waits only for chunk q's loads.
+  // Issuing every chunk up front let the compiler order chunk 0 last, and
+  // the first stage 1 then waited for the whole 200 KB tile.
+  constexpr int kLookahead = 3;
   float2 raw[L + 1][2][8];
 #pragma unroll
-  for (int q = 0; q < L + 1; ++q) {
+  for (int q = 0; q < kLookahead && q < L + 1; ++q) {
     load_item(q, it0, raw[q][0]);
     load_item(q, it1, raw[q][1]);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  if (tid < kN2) sTw8[tid] = tw8v;
+  if (tid < 2 * kN2) sTwp[tid] = conjf2(twpv);
 #pragma unroll
   for (int q = 0; q < L + 1; ++q) {
     float2* sTO = sT[q & 1];
     // stage 1: radix 8 over n2 = j1 + 8t (inputs already in registers)
     stage1_store(sTO, it0, raw[q][0]);
     stage1_store(sTO, it1, raw[q][1]);
+    __builtin_amdgcn_sched_barrier(0);
+    if (q + kLookahead < L + 1) {
+      load_item(q + kLookahead, it0, raw[q + kLookahead][0]);
+      load_item(q + kLookahead, it1, raw[q + kLookahead][1]);
+    }
     __syncthreads();
     // stage 2: twiddle W_64^(j2 t), radix 8; reads and writes rows j2 + 8t
     if (it0.live) stage2(sTO, it0, j2_0);
