@@ -61,9 +61,10 @@ enum cgconv_status {
  * batch >= 1; N >= 2 and a power of two, N <= CGCONV_NMAX; 0 <= L_max <=
  * CGCONV_LMAX; C >= 1.  Builds the sparse CG table (§4.3) and the FFT
  * twiddles on the host, allocates the device workspace (hipMalloc on the
- * current device, 2 * batch*N*(L_max+1)^2*C*8 bytes, plus 4 KiB per path for
- * the channel-mixing weights when L_max <= 6 and C <= 32) and uploads the
- * tables.
+ * current device: 2 * batch*N*(L_max+1)^2*C*8 bytes for the spectra, the
+ * gating partials, 8 * batch*ceil(N/64)*(L_max+1)*C bytes, 4 KiB per path
+ * for the channel-mixing weights when L_max <= 6 and C <= 32, and small
+ * tables; cgconv_plan_info reports the total) and uploads the tables.
  * Synchronous.  Returns NULL on failure (see cgconv_last_error()).
  */
 cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_t C);
