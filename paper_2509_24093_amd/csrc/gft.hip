@@ -78,17 +78,18 @@ constexpr int kTile = 128;  // block tile (rows and columns of C)
 constexpr int kStageBytes = 4 * 8192;  // A hi, A lo, B hi, B lo tiles of one 32-deep slice
 
 // Block computes a 128 x 128 tile of C with 4 waves of 64 x 64 (2 x 2 MFMA
-// tiles of 32 x 32).  The 32-deep slices of its A and B row tiles stream
-// through two LDS buffers (32 KB each): the copy of slice kt + 1 (one
-// global_load_lds per wave and KB) is in flight while slice kt is used.
+// tiles of 32 x 32).  The 32-deep slices of its A and B row tiles pass
+// through one 32 KB LDS buffer (one global_load_lds per wave and KB); three
+// blocks share a CU, so one block's MFMAs run while another waits for its
+// copy (measured slightly faster than two double-buffered blocks).
 // Lane l of a fragment holds row (or column) l % 32 and k values
 // 8 (l / 32) .. +7 of a 16-deep step; result register r of lane l is row
 // 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32 of the 32 x 32 tile.
 // Tiles are taken in bands of 4 row tiles, each XCD a contiguous run of the
 // band order, so the blocks in flight on one XCD share their A and B slices
 // in its L2.
-__global__ __launch_bounds__(256, 2) void gft_gemm_kernel(GftGemmArgs g, int Mt, int Nt, int per_xcd) {
-  __shared__ __attribute__((aligned(16))) char lds[2 * kStageBytes];
+__global__ __launch_bounds__(256, 3) void gft_gemm_kernel(GftGemmArgs g, int Mt, int Nt, int per_xcd) {
+  __shared__ __attribute__((aligned(16))) char lds[kStageBytes];
   const int b = blockIdx.y;
   const int id = blockIdx.x;
   const int t = (id & 7) * per_xcd + (id >> 3);  // tile index in band order
@@ -124,17 +125,11 @@ __global__ __launch_bounds__(256, 2) void gft_gemm_kernel(GftGemmArgs g, int Mt,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int fr = lane & 31, fc = lane >> 5;
-  copy_slice(0, 0);
   for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) {
-      copy_slice(kt + 1, buf ^ 1);
-      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // this wave's copies of slice kt have landed
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
-    __syncthreads();  // every wave's copies of slice kt are visible
-    const char* st = lds + buf * kStageBytes;
+    copy_slice(kt, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's copies of slice kt have landed
+    __syncthreads();                                   // every wave's copies are visible
+    const char* st = lds;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int c = 2 * s + fc;  // k chunk of this lane's 8 values
@@ -156,7 +151,7 @@ __global__ __launch_bounds__(256, 2) void gft_gemm_kernel(GftGemmArgs g, int Mt,
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_l[i], b_h[j], acc[i][j], 0, 0, 0);
         }
     }
-    __syncthreads();  // slice kt is consumed before its buffer is refilled
+    __syncthreads();  // slice kt is consumed before the buffer is refilled
   }
   const int m0 = tm * kTile + wm * 64, n0 = tn * kTile + wn * 64;
   float* c = g.c + b * g.c_bs;
