@@ -12,8 +12,9 @@
 // accumulation.
 //
 // gft_split_kernel  fp32 matrix -> zero-padded hi / lo operand arrays in the
-//                   tiled k-contiguous layout the GEMM reads (optionally
-//                   transposed, through a 32 x 32 LDS tile);
+//                   tiled k-contiguous layout the GEMM reads: its transpose,
+//                   and for a square basis also the matrix as is, from one
+//                   read of it staged through LDS;
 // gft_gemm_kernel   C[m][n] = sum_k A[m][k] Bt[n][k] with A, Bt in the tiled
 //                   layout, streamed through LDS by direct copies.
 #include <hip/hip_runtime.h>
@@ -42,34 +43,70 @@ __device__ __forceinline__ long long tiled_offset(int o, int kk, int Kp) {
   return ((long long)((o >> 7) * (Kp >> 5) + (kk >> 5)) * 4 + ((kk & 31) >> 3)) * 1024 + (o & 127) * 8 + (kk & 7);
 }
 
-// dst[o][kk] (tiled layout) for o < dst_rows, kk < dst_cols (= Kp), from
-// src[kk][o] (TRANSPOSE) or src[o][kk], zero outside src_rows x src_cols.
-// Block = 32 x 8 threads over a 32 x 32 tile of dst.
-template <bool TRANSPOSE>
+// Split of a source block into the tiled layout.  A block stages a 32 x 128
+// block of src (rows r0.., columns c0..; zero outside src_rows x src_cols)
+// in LDS with coalesced row reads, then writes 8 consecutive k values per
+// lane as one 16-byte store per part, consecutive lanes on consecutive rows
+// of one 8-k chunk (512 B to 1 KB contiguous per wave):
+//   transposed  a.hi / a.lo:       dst[o][kk] = src[kk][o], o = c0 + 0..127,
+//                                  kk = r0 + 0..31;
+//   plain (BOTH) a.hi_p / a.lo_p:  dst[o][kk] = src[o][kk], o = r0 + 0..31,
+//                                  kk = c0 + 0..127.
+// Both outputs are dst_rows x dst_cols; stores with kk >= dst_cols are skipped
+// (dst_rows is a multiple of 128 and the grid stays inside it).
+constexpr int kSplitR = 32, kSplitC = 128, kSplitPitch = kSplitC + 1;
+
+__device__ __forceinline__ void store_split8(uint16_t* hi, uint16_t* lo, long long off, const float* x) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t h0 = bf16_rne(x[2 * j]), h1 = bf16_rne(x[2 * j + 1]);
+    const uint32_t l0 = bf16_rne(x[2 * j] - __uint_as_float(h0 << 16));
+    const uint32_t l1 = bf16_rne(x[2 * j + 1] - __uint_as_float(h1 << 16));
+    h[j] = h0 | (h1 << 16);
+    l[j] = l0 | (l1 << 16);
+  }
+  *reinterpret_cast<uint4*>(hi + off) = make_uint4(h[0], h[1], h[2], h[3]);
+  *reinterpret_cast<uint4*>(lo + off) = make_uint4(l[0], l[1], l[2], l[3]);
+}
+
+template <bool BOTH>
 __global__ __launch_bounds__(256) void gft_split_kernel(GftSplitArgs a) {
-  __shared__ float tile[32][33];
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  const int kk0 = blockIdx.x * 32, o0 = blockIdx.y * 32;
+  __shared__ float S[kSplitR][kSplitPitch];
+  const int t = threadIdx.x;
+  const int c0 = blockIdx.x * kSplitC, r0 = blockIdx.y * kSplitR;
   const float* src = a.src + (long long)blockIdx.z * a.src_bs;
   const long long db = (long long)blockIdx.z * a.dst_bs;
-  for (int y = ty; y < 32; y += 8) {
-    if (TRANSPOSE) {  // read rows kk0.. of src (coalesced along o)
-      const int sr = kk0 + y, sc = o0 + tx;
-      tile[y][tx] = (sr < a.src_rows && sc < a.src_cols) ? src[(long long)sr * a.ld + sc] : 0.f;
-    } else {          // read rows o0.. of src (coalesced along kk)
-      const int sr = o0 + y, sc = kk0 + tx;
-      tile[tx][y] = (sr < a.src_rows && sc < a.src_cols) ? src[(long long)sr * a.ld + sc] : 0.f;
+  {
+    const int cl = t & 127, c = c0 + cl;
+#pragma unroll
+    for (int i = 0; i < kSplitR / 2; ++i) {
+      const int rl = 2 * i + (t >> 7), r = r0 + rl;
+      S[rl][cl] = (r < a.src_rows && c < a.src_cols) ? src[(long long)r * a.ld + c] : 0.f;
     }
   }
   __syncthreads();
-  for (int y = ty; y < 32; y += 8) {
-    const int o = o0 + y, kk = kk0 + tx;
+  float x[8];
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {  // transposed: item (o = c0 + j, chunk ch of kk = r0 ..)
+    const int j = t & 127, ch = (t >> 7) + 2 * it;
+    const int o = c0 + j, kk = r0 + 8 * ch;
     if (o < a.dst_rows && kk < a.dst_cols) {
-      const float x = tile[tx][y];  // element (o, kk)
-      const uint32_t h = bf16_rne(x);
-      const long long off = db + tiled_offset(o, kk, a.dst_cols);
-      a.hi[off] = (uint16_t)h;
-      a.lo[off] = (uint16_t)bf16_rne(x - __uint_as_float(h << 16));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = S[8 * ch + e][j];
+      store_split8(a.hi, a.lo, db + tiled_offset(o, kk, a.dst_cols), x);
+    }
+  }
+  if (BOTH) {
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {  // plain: item (o = r0 + r, chunk cc of kk = c0 ..)
+      const int r = t & 31, cc = (t >> 5) + 8 * it;
+      const int o = r0 + r, kk = c0 + 8 * cc;
+      if (o < a.dst_rows && kk < a.dst_cols) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = S[r][8 * cc + e];
+        store_split8(a.hi_p, a.lo_p, db + tiled_offset(o, kk, a.dst_cols), x);
+      }
     }
   }
 }
@@ -170,10 +207,16 @@ __global__ __launch_bounds__(256, 3) void gft_gemm_kernel(GftGemmArgs g, int Mt,
 
 }  // namespace
 
-hipError_t launch_gft_split(const GftSplitArgs& a, bool transpose, int batch, hipStream_t s) {
-  if (!a.src || !a.hi || !a.lo || a.dst_rows <= 0 || a.dst_cols <= 0 || batch <= 0) return hipErrorInvalidValue;
-  const dim3 grid((a.dst_cols + 31) / 32, (a.dst_rows + 31) / 32, batch);
-  if (transpose)
+hipError_t launch_gft_split(const GftSplitArgs& a, int batch, hipStream_t s) {
+  const bool both = a.hi_p != nullptr;
+  if (!a.src || !a.hi || !a.lo || (both && !a.lo_p) || a.dst_rows <= 0 || a.dst_rows % 128 != 0 ||
+      a.dst_cols <= 0 || a.dst_cols % 32 != 0 || (both && a.dst_rows < a.dst_cols) || batch <= 0)
+    return hipErrorInvalidValue;
+  // columns of src: o of the transposed output (< dst_rows), and kk of the
+  // plain one (< dst_cols <= dst_rows); rows of src: kk of the transposed
+  // output, and o of the plain one
+  const dim3 grid(a.dst_rows / kSplitC, (both ? a.dst_rows : a.dst_cols) / kSplitR, batch);
+  if (both)
     hipLaunchKernelGGL(gft_split_kernel<true>, grid, dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL(gft_split_kernel<false>, grid, dim3(256), 0, s, a);

@@ -135,13 +135,15 @@ struct GftSplitArgs {
   const float* src;     // fp32 [src_rows][ld] per batch element (valid: src_rows x src_cols)
   long long src_bs;     // elements per batch element
   int ld, src_rows, src_cols;
-  uint16_t* hi;         // [dst_rows][dst_cols] per batch element
+  uint16_t* hi;         // transpose of src: [dst_rows][dst_cols] per batch element
   uint16_t* lo;
-  long long dst_bs;
-  int dst_rows, dst_cols;
+  uint16_t* hi_p;       // src as is (square src, dst_rows >= dst_cols), or nullptr
+  uint16_t* lo_p;
+  long long dst_bs;     // elements per batch element, both outputs
+  int dst_rows, dst_cols;  // multiples of 128 and 32
 };
-// transpose: dst[o][kk] = src[kk][o]; else dst[o][kk] = src[o][kk]
-hipError_t launch_gft_split(const GftSplitArgs& a, bool transpose, int batch, hipStream_t s);
+// hi / lo: dst[o][kk] = src[kk][o]; hi_p / lo_p (if set): dst[o][kk] = src[o][kk]
+hipError_t launch_gft_split(const GftSplitArgs& a, int batch, hipStream_t s);
 // C[m][n] = sum_k A[m][k] Bt[n][k]; A: [Mp][Kp], Bt: [Np][Kp] (hi / lo each);
 // rows m < M and columns n < N of C are stored (row stride ldc)
 struct GftGemmArgs {
