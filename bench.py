@@ -107,6 +107,27 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}), flush=True)
 
 
+def copy_peak_gbs(nbytes=1 << 30, reps=10):
+    """Measured HBM ceiling: bytes read plus written per second by a plain
+    device-to-device copy of nbytes on the current stream (HIP events on that
+    stream, after warm-up copies)."""
+    import torch
+    src = torch.ones(nbytes // 4, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
 def cpu_baseline(q, k, L, budget_s, got, linear=False):
     """Oracle direct mode on sampled output rows; returns the bench object and
     the parity of the GPU output on those rows."""
@@ -122,10 +143,11 @@ def cpu_baseline(q, k, L, budget_s, got, linear=False):
     rng = np.random.default_rng(2024)
     # rows in chunks of 8 per batch element, cycling over b, until the budget
     # is spent; (0, 0) and (B-1, N-1) are always included
-    rows, ref = [], []
+    rows, ref, chunk_s = [], [], []
     t0 = time.perf_counter()
     chunk = 0
     while True:
+        tc = time.perf_counter()
         b = chunk % B
         picks = [int(x) for x in rng.integers(0, N, size=8)]
         if chunk == 0:
@@ -135,21 +157,28 @@ def cpu_baseline(q, k, L, budget_s, got, linear=False):
         part = [(b, i) for i in picks]
         ref.extend(rows_fn(q, k, L, part))
         rows.extend(part)
+        chunk_s.append(time.perf_counter() - tc)
         chunk += 1
         if time.perf_counter() - t0 >= budget_s and chunk >= B:
             break
     dt = time.perf_counter() - t0
     R = len(rows)
+    # three consecutive thirds of the chunks timed as separate runs; the
+    # reported rate is their median
+    thirds = [chunk_s[i * len(chunk_s) // 3:(i + 1) * len(chunk_s) // 3] for i in range(3)]
+    rates = sorted(8 * len(t) / sum(t) for t in thirds if t)
     num = den = 0.0
     for n, (b, i) in enumerate(rows):
         d = got[b, i].astype(np.float64) - ref[n]
         num += float((d * d).sum())
         den += float((ref[n] * ref[n]).sum())
     cores = len(os.sched_getaffinity(0))
-    obj = {"value": R / dt, "unit": "tokens/s", "cores": blas_threads or cores, "kind": "oracle",
+    value = rates[len(rates) // 2] if rates else R / dt
+    obj = {"value": value, "unit": "tokens/s", "cores": blas_threads or cores, "kind": "oracle",
            "sample": f"direct O(N^2) definition on {R} sampled output rows (b, i) of the same workload "
-                     f"(all K components and C channels per row), fp64 numpy, {dt:.1f} s; "
-                     f"host exposes {cores} cores"}
+                     f"(all K components and C channels per row), fp64 numpy, {dt:.1f} s; median of "
+                     f"three runs of {len(chunk_s) // 3}+ chunks of 8 rows "
+                     f"({', '.join(f'{r:.2f}' for r in rates)} rows/s); host exposes {cores} cores"}
     return obj, (num / den) ** 0.5 if den > 0 else 0.0, R
 
 
@@ -303,6 +332,10 @@ def main():
     roofline = cg_roofline(stage_avg, B, Nf, L, C, n_products, nnz,
                            counters["cg_hbm_bytes_per_launch"] if counters else None, traffic_src)
     hbm_alg_gbs = 3 * S / (ms * 1e-3) / 1e9
+    copy_gbs = copy_peak_gbs()
+    log(f"[bench] device copy of 1 GiB: {copy_gbs:.0f} GB/s")
+    for st in stages.values():
+        st["frac_of_copy"] = round(st["gbs"] / copy_gbs, 4) if st.get("bytes") else None
     result = {
         "metric": METRIC if args.boundary == "cyclic" else METRIC_LINEAR,
         "value": tokens / (ms * 1e-3),
@@ -323,6 +356,9 @@ def main():
                 "counter_bytes_per_step": counters["step_hbm_bytes"] if counters else None,
                 "counter_gbs": round(counters["step_hbm_bytes"] / (ms * 1e-3) / 1e9, 1) if counters else None,
                 "counter_frac": round(counters["step_hbm_bytes"] / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4)
+                if counters else None,
+                "copy_measured_gbs": round(copy_gbs, 1), "frac_of_copy": round(hbm_alg_gbs / copy_gbs, 4),
+                "counter_frac_of_copy": round(counters["step_hbm_bytes"] / (ms * 1e-3) / 1e9 / copy_gbs, 4)
                 if counters else None},
         "roofline": roofline,
         "stages": stages,
