@@ -694,7 +694,8 @@ int run_graph(cgconv_plan* p, const float* U, const float* x1, const float* x2, 
   const int B = (int)p->B, n = (int)p->N, KC = p->K * (int)p->C;
   const int Kp = (int)p->Kp, Mp = (int)p->Mp, KCp = (int)p->KCp;
   auto split = [&](const float* src, long long src_bs, int ld, int rows, int cols, uint16_t* hi, uint16_t* lo,
-                   long long dst_bs, int dst_rows, uint16_t* hi_p = nullptr, uint16_t* lo_p = nullptr) {
+                   long long dst_bs, int dst_rows, int row0, int dst_rt, uint16_t* hi_p = nullptr,
+                   uint16_t* lo_p = nullptr) {
     GftSplitArgs a;
     a.src = src;
     a.src_bs = src_bs;
@@ -708,6 +709,8 @@ int run_graph(cgconv_plan* p, const float* U, const float* x1, const float* x2, 
     a.dst_bs = dst_bs;
     a.dst_rows = dst_rows;
     a.dst_cols = Kp;
+    a.row0 = row0;
+    a.dst_rt = dst_rt;
     return launch_gft_split(a, B, stream);
   };
   auto gemm = [&](const uint16_t* ah, const uint16_t* al, const uint16_t* bh, const uint16_t* bl, long long b_bs,
@@ -732,14 +735,15 @@ int run_graph(cgconv_plan* p, const float* U, const float* x1, const float* x2, 
   mark();
   // A operands: U^T (rows = graph frequencies) and U (rows = nodes), k = the other index
   if (split_u) {  // U^T and U from one read of U
-    if ((e = split(U, nn, n, n, n, p->ga_fh, p->ga_fl, (long long)Mp * Kp, Mp, p->ga_ih, p->ga_il)) != hipSuccess)
+    if ((e = split(U, nn, n, n, n, p->ga_fh, p->ga_fl, (long long)Mp * Kp, Mp, 0, Mp / 128, p->ga_ih, p->ga_il)) !=
+        hipSuccess)
       goto fail;
   }
   mark();
   // B operand of the forward transform: [q | k] transposed, q in rows 0..KC-1, k from row KCp
-  if ((e = split(x1, xbs, KC, n, KC, p->gb_fh, p->gb_fl, 2LL * KCp * Kp, KCp)) != hipSuccess) goto fail;
-  if ((e = split(x2, xbs, KC, n, KC, p->gb_fh + (size_t)KCp * Kp, p->gb_fl + (size_t)KCp * Kp, 2LL * KCp * Kp,
-                 KCp)) != hipSuccess)
+  if ((e = split(x1, xbs, KC, n, KC, p->gb_fh, p->gb_fl, 2LL * KCp * Kp, KCp, 0, 2 * KCp / 128)) != hipSuccess)
+    goto fail;
+  if ((e = split(x2, xbs, KC, n, KC, p->gb_fh, p->gb_fl, 2LL * KCp * Kp, KCp, KCp, 2 * KCp / 128)) != hipSuccess)
     goto fail;
   mark();
   // [q_hat | k_hat] = U^T [q | k]
@@ -762,7 +766,8 @@ int run_graph(cgconv_plan* p, const float* U, const float* x1, const float* x2, 
     if ((e = launch_product(p->L, a, stream)) != hipSuccess) goto fail;
   }
   mark();
-  if ((e = split(p->g_uhat, xbs, KC, n, KC, p->gb_ih, p->gb_il, (long long)KCp * Kp, KCp)) != hipSuccess)
+  if ((e = split(p->g_uhat, xbs, KC, n, KC, p->gb_ih, p->gb_il, (long long)KCp * Kp, KCp, 0, KCp / 128)) !=
+      hipSuccess)
     goto fail;
   mark();
   // u = U u_hat, written straight into out ([B][n][K][C] = [B][n][KC])

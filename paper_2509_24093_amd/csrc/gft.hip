@@ -32,15 +32,18 @@ __device__ __forceinline__ uint32_t bf16_rne(float x) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Tiled operand layout: an operand X[rows][Kp] (rows a multiple of 128, Kp
-// of 32) is stored as tiles of 128 rows x 32 k, tile (rt, kt) at
-// ((rt * Kp/32 + kt) * 4096) elements, inside a tile [chunk c = k%32 / 8]
+// Tiled operand layout: an operand X[rows][Kp] (rows = RT * 128, Kp a
+// multiple of 32) is stored as tiles of 128 rows x 32 k, tile (rt, kt) at
+// ((kt * RT + rt) * 4096) elements, inside a tile [chunk c = k%32 / 8]
 // [row r % 128][k % 8].  A tile is 8 KB of contiguous bf16 (one per hi /
 // lo part), so the GEMM copies it to LDS with fully coalesced 16-byte
 // lanes, and a fragment read (32 rows of one 8-value chunk) is 512
-// contiguous bytes of LDS.
-__device__ __forceinline__ long long tiled_offset(int o, int kk, int Kp) {
-  return ((long long)((o >> 7) * (Kp >> 5) + (kk >> 5)) * 4 + ((kk & 31) >> 3)) * 1024 + (o & 127) * 8 + (kk & 7);
+// contiguous bytes of LDS.  The tiles of one 32-deep slice kt are
+// contiguous across row tiles: the slices the blocks in flight read at one
+// time form one run of addresses instead of lines 1 MB apart, which spread
+// over every L2 channel.
+__device__ __forceinline__ long long tiled_offset(int o, int kk, int RT) {
+  return ((long long)((kk >> 5) * RT + (o >> 7)) * 4 + ((kk & 31) >> 3)) * 1024 + (o & 127) * 8 + (kk & 7);
 }
 
 // Split of a source block into the tiled layout.  A block stages a 32 x 128
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(256) void gft_split_kernel(GftSplitArgs a) {
     if (o < a.dst_rows && kk < a.dst_cols) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[e] = S[8 * ch + e][j];
-      store_split8(a.hi, a.lo, db + tiled_offset(o, kk, a.dst_cols), x);
+      store_split8(a.hi, a.lo, db + tiled_offset(a.row0 + o, kk, a.dst_rt), x);
     }
   }
   if (BOTH) {
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(256) void gft_split_kernel(GftSplitArgs a) {
       if (o < a.dst_rows && kk < a.dst_cols) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) x[e] = S[r][8 * cc + e];
-        store_split8(a.hi_p, a.lo_p, db + tiled_offset(o, kk, a.dst_cols), x);
+        store_split8(a.hi_p, a.lo_p, db + tiled_offset(a.row0 + o, kk, a.dst_rt), x);
       }
     }
   }
@@ -137,16 +140,16 @@ __global__ __launch_bounds__(256, 3) void gft_gemm_kernel(GftGemmArgs g, int Mt,
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int KT = g.Kp >> 5;
-  // this block's A and B row tiles (8 KB per 32-deep slice, slices contiguous)
-  const uint16_t* srcs[4] = {g.ah + b * g.a_bs + (long long)tm * kTile * g.Kp,
-                             g.al + b * g.a_bs + (long long)tm * kTile * g.Kp,
-                             g.bh + b * g.b_bs + (long long)tn * kTile * g.Kp,
-                             g.bl + b * g.b_bs + (long long)tn * kTile * g.Kp};
+  // this block's A and B row tiles: 8 KB per 32-deep slice, slice kt of row
+  // tile r at (kt * (row tiles) + r) * 8 KB
+  const uint16_t* srcs[4] = {g.ah + b * g.a_bs + tm * 4096, g.al + b * g.a_bs + tm * 4096,
+                             g.bh + b * g.b_bs + tn * 4096, g.bl + b * g.b_bs + tn * 4096};
+  const long long sstride[2] = {(long long)Mt * 4096, (long long)Nt * 4096};
   auto copy_slice = [&](int kt, int buf) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int ch = wave + 4 * i;  // KB chunk of the 32 KB stage: part ch / 8, KB ch % 8
-      const uint16_t* src = srcs[ch >> 3] + (long long)kt * 4096 + (ch & 7) * 512 + lane * 8;
+      const uint16_t* src = srcs[ch >> 3] + kt * sstride[ch >> 4] + (ch & 7) * 512 + lane * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
                                        (__attribute__((address_space(3))) void*)(lds + buf * kStageBytes + ch * 1024),
                                        16, 0, 0);
@@ -210,7 +213,9 @@ __global__ __launch_bounds__(256, 3) void gft_gemm_kernel(GftGemmArgs g, int Mt,
 hipError_t launch_gft_split(const GftSplitArgs& a, int batch, hipStream_t s) {
   const bool both = a.hi_p != nullptr;
   if (!a.src || !a.hi || !a.lo || (both && !a.lo_p) || a.dst_rows <= 0 || a.dst_rows % 128 != 0 ||
-      a.dst_cols <= 0 || a.dst_cols % 32 != 0 || (both && a.dst_rows < a.dst_cols) || batch <= 0)
+      a.dst_cols <= 0 || a.dst_cols % 32 != 0 || (both && a.dst_rows < a.dst_cols) || batch <= 0 ||
+      a.row0 < 0 || a.row0 % 128 != 0 || a.row0 + a.dst_rows > 128LL * a.dst_rt ||
+      (long long)a.dst_bs < 128LL * a.dst_rt * a.dst_cols)
     return hipErrorInvalidValue;
   // columns of src: o of the transposed output (< dst_rows), and kk of the
   // plain one (< dst_cols <= dst_rows); rows of src: kk of the transposed

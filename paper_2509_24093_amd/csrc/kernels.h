@@ -135,12 +135,13 @@ struct GftSplitArgs {
   const float* src;     // fp32 [src_rows][ld] per batch element (valid: src_rows x src_cols)
   long long src_bs;     // elements per batch element
   int ld, src_rows, src_cols;
-  uint16_t* hi;         // transpose of src: [dst_rows][dst_cols] per batch element
-  uint16_t* lo;
+  uint16_t* hi;         // transpose of src: rows row0 .. row0 + dst_rows - 1 of a
+  uint16_t* lo;         // [128 dst_rt][dst_cols] tiled matrix per batch element
   uint16_t* hi_p;       // src as is (square src, dst_rows >= dst_cols), or nullptr
   uint16_t* lo_p;
-  long long dst_bs;     // elements per batch element, both outputs
+  long long dst_bs;     // elements per batch element, both outputs (>= 128 dst_rt dst_cols)
   int dst_rows, dst_cols;  // multiples of 128 and 32
+  int row0, dst_rt;        // first row written (a multiple of 128); row tiles of the whole matrix
 };
 // hi / lo: dst[o][kk] = src[kk][o]; hi_p / lo_p (if set): dst[o][kk] = src[o][kk]
 hipError_t launch_gft_split(const GftSplitArgs& a, int batch, hipStream_t s);
