@@ -28,6 +28,7 @@
 
 #include "cgconv.h"
 #include "cg_table.h"
+#include "gft.h"
 #include "kernels.h"
 
 using namespace cgconv;

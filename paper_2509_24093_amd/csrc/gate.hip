@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include "cg_common.h"
+#include "gft.h"
 
 namespace cgconv {
 namespace cgdev {

@@ -19,6 +19,7 @@
 //                   layout, streamed through LDS by direct copies.
 #include <hip/hip_runtime.h>
 
+#include "gft.h"
 #include "kernels.h"
 
 namespace cgconv {
