@@ -147,7 +147,7 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
  *
  * cgconv_plan_create_graph(batch, N, L_max, C): N = nodes per batch element,
  * 1 <= N <= CGCONV_GRAPH_NMAX (any N); allocates the split operands of the
- * two transforms (about 16 batch*N^2 + 24 batch*N*K*C bytes).  Such a plan
+ * two transforms (about 8 batch*N^2 + 24 batch*N*K*C bytes).  Such a plan
  * serves cgconv_forward_graph, cgconv_backward_graph and cgconv_gate_value
  * only.
  * cgconv_forward_graph: U DEVICE fp32 [batch][N][N] (row i = node, column f
