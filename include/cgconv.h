@@ -268,7 +268,7 @@ int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, 
  * summed time of each stage in milliseconds to ms[0 .. min(cap, n_stages)-1];
  * n_stages and n_calls (may be NULL) receive the stage count (3 for N <= 256:
  * fft_fwd, cg, fft_inv; 5 above: fft_fwd_1, fft_fwd_2, cg, fft_inv_1,
- * fft_inv_2; for plans with 512 <= N <= 16384 and L_max <= 6: fft_fwd_1,
+ * fft_inv_2; for plans with 512 <= N <= 32768 and L_max <= 6: fft_fwd_1,
  * cg_fused, fft_inv_2) and the number of timed calls.  The first timed call
  * fixes which kind is timed: plain forwards, mixed forwards (cg_mix replaces
  * cg and the unfused passes are listed), backwards (each of the two

@@ -12,7 +12,7 @@
 //     I1  for each w1: inverse length-N2 DFT, twiddle W_N^(-n2 w1)   W -> V
 //     I2  for each n2: inverse length-N1 DFT, x 1/N, split channels  V -> out
 // Y, Z, W, V live in two plan-owned workspaces of B*N*K*C float2 each.
-//   512 <= N <= 16384, L_max <= 6: N2 = 64 and F2 + CG + I1 run as one fused
+//   512 <= N <= 32768, L_max <= 6: N2 = 64 and F2 + CG + I1 run as one fused
 //   kernel (cg_fused.hip) between F1 and I2; the spectra stay on chip.
 #include <hip/hip_runtime.h>
 
@@ -496,7 +496,7 @@ cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32
   const char* unfused = std::getenv("CGCONV_UNFUSED");
   // the fused kernel addresses one batch element's spectra with 32-bit byte offsets
   const bool fits32 = (long double)N * K * C * 8 < 4294967296.0L;
-  if (N >= 512 && N <= 16384 && L_max <= kFusedLmax && fits32 && !(unfused && unfused[0] == '1') &&
+  if (N >= 512 && N <= 32768 && L_max <= kFusedLmax && fits32 && !(unfused && unfused[0] == '1') &&
       !p->force_generic) {
     p->fused = true;
     p->N2 = 64;

@@ -2,14 +2,14 @@
 //
 // The features are stored [batch][N][K][C] with channels fastest, so a
 // signal (fixed b, component, channel) runs down a column with stride K*C.
-// Each pass transforms R rows (R <= 256) of a tile of G adjacent columns:
+// Each pass transforms R rows (R <= 512) of a tile of G adjacent columns:
 // every global access of a wavefront covers G consecutive columns of one row,
 // i.e. one contiguous segment of G*8 bytes (complex) or G*4 bytes (real), so
 // HBM reads and writes are coalesced without any transpose.  Inside a block
 // the length-R DFT is a two-stage Stockham factorisation R = R1 * R2: stage 1
 // reads its R1 inputs straight from HBM into registers and runs a radix-R1
 // DFT there, the R x G tile is exchanged once through LDS, stage 2 runs a
-// radix-R2 DFT in registers and writes straight to HBM.  Lengths above 256
+// radix-R2 DFT in registers and writes straight to HBM.  Longer transforms
 // use two passes (four-step factorisation, see the plan).
 #include <hip/hip_runtime.h>
 
@@ -197,7 +197,11 @@ __global__ __launch_bounds__(T) void fft_pass_kernel(PassArgs a) {
       finish_item(x1, cl + 1, j1, col + 1, ok);
     }
   } else {
-    for (int it = threadIdx.x; it < G * (R / R1); it += T) {
+    constexpr int NIT = (G * (R / R1) + T - 1) / T;  // items per thread, unrolled so
+#pragma unroll                                          // their loads can overlap
+    for (int rep = 0; rep < NIT; ++rep) {
+      const int it = threadIdx.x + rep * T;
+      if (NIT * T != G * (R / R1) && it >= G * (R / R1)) break;
       const int cl = it % G, j1 = it / G;
       const int col = col0 + cl;
       const bool ok = col < a.W;
@@ -252,14 +256,18 @@ __global__ __launch_bounds__(T) void fft_pass_kernel(PassArgs a) {
 // two-stage passes up to R = 128.  R = 256 keeps wide rows instead: 32
 // complex columns (256 B) with 512 threads and 64 KB, and for the real pair
 // input 64 columns (256 B of q and of k per row) with 1024 threads and
-// 128 KB (measured at the point-cloud shape: 0.95 -> 0.66 ms).
+// 128 KB (measured at the point-cloud shape: 0.95 -> 0.66 ms).  R = 512
+// (radix 16 x 32, the first and last pass of the fused pipeline at N =
+// 32768) takes 32 columns and 128 KB with 512 threads, two stage-1 items per
+// thread (1024 threads spill the radix-32 stage out of their 128 registers:
+// 1.56 -> 1.24 ms for the first pass of the zero-padded point-cloud shape).
 template <int R, int INM>
 constexpr int tile_cols() {
-  return R <= 16 ? kThreads : (R == 256 ? (INM == IN_COMPLEX ? 32 : 64) : 4096 / R);
+  return R <= 16 ? kThreads : (R == 512 ? 32 : (R == 256 ? (INM == IN_COMPLEX ? 32 : 64) : 4096 / R));
 }
 template <int R, int INM>
 constexpr int tile_threads() {
-  return R == 256 ? (INM == IN_COMPLEX ? 512 : 1024) : kThreads;
+  return R == 512 ? 512 : (R == 256 ? (INM == IN_COMPLEX ? 512 : 1024) : kThreads);
 }
 
 template <int R, int INM, int OUTM, int DIR>
@@ -284,6 +292,7 @@ hipError_t launch_modes(const PassDesc& d, hipStream_t s) {
     case 64: return launch_r<64, INM, OUTM, DIR>(d, s);
     case 128: return launch_r<128, INM, OUTM, DIR>(d, s);
     case 256: return launch_r<256, INM, OUTM, DIR>(d, s);
+    case 512: return launch_r<512, INM, OUTM, DIR>(d, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -59,10 +59,10 @@ def test_small_workloads_against_direct(name):
     assert eq <= TOL and ek <= TOL
 
 
-# (B, N, L, C): single pass (N <= 256), fused two-pass (512 <= N <= 16384,
-# L <= 6), unfused two-pass (L >= 7, or N > 16384); odd C and C = 1
+# (B, N, L, C): single pass (N <= 256), fused two-pass (512 <= N <= 32768,
+# L <= 6), unfused two-pass (L >= 7, or N > 32768); odd C and C = 1
 SHAPES = [(1, 2, 2, 1), (2, 16, 6, 3), (1, 256, 8, 2), (2, 512, 4, 5), (1, 2048, 6, 2), (1, 4096, 1, 33),
-          (1, 1024, 7, 3), (1, 32768, 2, 2), (3, 64, 0, 4)]
+          (1, 1024, 7, 3), (1, 32768, 2, 2), (1, 32768, 5, 3), (1, 65536, 1, 2), (3, 64, 0, 4)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dN%dL%dC%d" % s)

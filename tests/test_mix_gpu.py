@@ -69,10 +69,11 @@ def test_mixed_small_workloads(name):
     assert err < TOL
 
 
-# (B, N, L, C): N <= 256 single pass; 512..16384 the shapes of fused plans
-# (mixing runs the unfused passes there); 32768 the plain two-pass split.
+# (B, N, L, C): N <= 256 single pass; 512..32768 the shapes of fused plans
+# (mixing runs the unfused passes there with N2 = 64: radix-512 outer passes
+# at 32768); 65536 the plain two-pass split.
 SHAPES = [(1, 64, 0, 1), (2, 128, 1, 3), (3, 256, 2, 5), (1, 512, 6, 32), (2, 1024, 4, 16),
-          (1, 2048, 5, 7), (1, 32768, 2, 2), (5, 16, 3, 32), (1, 2, 6, 9)]
+          (1, 2048, 5, 7), (1, 32768, 2, 2), (1, 65536, 1, 3), (5, 16, 3, 32), (1, 2, 6, 9)]
 
 
 @pytest.mark.parametrize("B,N,L,C", SHAPES)

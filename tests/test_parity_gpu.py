@@ -101,13 +101,15 @@ def test_small_workloads_bf16(name):
     assert err <= TOL_BF16
 
 
-# (B, N, L, C): single-pass lengths 2..256, two-pass 512..65536, every
+# (B, N, L, C): single-pass lengths 2..256, two-pass 512..65536 (fused up
+# to 32768 at L <= 6, whose outer passes are radix 512 at 32768), every
 # generated L (0..8), odd C and C = 1,
 # column counts K*C spanning several tiles with a ragged tail.
 SHAPES = [
     (1, 2, 2, 1), (3, 4, 1, 3), (2, 8, 3, 2), (1, 16, 6, 5), (2, 32, 4, 7), (1, 64, 0, 1),
     (1, 128, 5, 6), (2, 256, 6, 3), (1, 512, 2, 9), (2, 1024, 3, 37), (1, 2048, 6, 2),
-    (1, 4096, 1, 33), (1, 8192, 2, 3), (1, 65536, 1, 2), (1, 64, 7, 3), (2, 512, 8, 2),
+    (1, 4096, 1, 33), (1, 8192, 2, 3), (1, 32768, 6, 3), (2, 32768, 2, 5), (1, 65536, 1, 2), (1, 64, 7, 3),
+    (2, 512, 8, 2),
 ]
 
 
@@ -249,12 +251,12 @@ def test_argument_errors_on_gpu():
         del os.environ["CGCONV_TEST_FAIL_ALLOC"]
 
 
-# Shapes on the fused pipeline (512 <= N <= 16384, L <= 6): C = 1, L = 0,
+# Shapes on the fused pipeline (512 <= N <= 32768, L <= 6): C = 1, L = 0,
 # channel counts that leave a ragged last block of 4, both ends of the N
 # range.  The fused result must agree with the modular pipeline and with
 # the oracle.
 FUSED_SHAPES = [(2, 512, 4, 1), (1, 16384, 0, 3), (3, 1024, 6, 4), (1, 2048, 5, 7), (2, 4096, 3, 2),
-                (1, 8192, 1, 5)]
+                (1, 8192, 1, 5), (1, 32768, 4, 5)]
 
 
 @pytest.mark.parametrize("shape", FUSED_SHAPES, ids=lambda s: "B%dN%dL%dC%d" % s)
@@ -281,7 +283,8 @@ def test_fused_bf16():
 @pytest.mark.parametrize("N,L,expect", [(256, 3, ["fft_fwd", "cg", "fft_inv"]),
                                         (1024, 3, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
                                         (16384, 6, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
-                                        (32768, 2, ["fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"]),
+                                        (32768, 2, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
+                                        (65536, 2, ["fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"]),
                                         (1024, 7, ["fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"])])
 def test_plan_picks_pipeline(N, L, expect):
     torch = _torch()
