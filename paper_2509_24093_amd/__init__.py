@@ -398,3 +398,34 @@ class GraphPlan(Plan):
         return gq, gk
 
     __call__ = forward
+
+
+_graph_fn = None
+
+
+def cgconv_graph(U, q, k, plan: GraphPlan):
+    """Differentiable graph CG convolution of fp32 tensors in q and k: the
+    forward and the backward are the plan's cgconv_forward_graph and
+    cgconv_backward_graph.  U is a constant here (no gradient flows to it)."""
+    global _graph_fn
+    if getattr(U, "requires_grad", False):
+        raise ValueError("cgconv_graph gives no gradient with respect to U; pass U.detach()")
+    if _graph_fn is None:
+        import torch
+
+        class _GraphFn(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, U, q, k, plan):
+                ctx.save_for_backward(U, q, k)
+                ctx.plan = plan
+                return plan.forward(U, q, k)
+
+            @staticmethod
+            def backward(ctx, grad_out):
+                U, q, k = ctx.saved_tensors
+                gq, gk = ctx.plan.backward(U, q, k, grad_out.contiguous(), need_q=ctx.needs_input_grad[1],
+                                           need_k=ctx.needs_input_grad[2])
+                return None, gq, gk, None
+
+        _graph_fn = _GraphFn
+    return _graph_fn.apply(U, q, k, plan)

@@ -9,7 +9,8 @@ Gaussian matrices) for node counts that are and are not multiples of the
 eigenbasis with the node-permutation property checked on the GPU output;
 the graph workload at full size (B=4, N=4096, L=6, C=32) on a channel
 subset (channels are independent); the backward (orthonormal and general
-bases, a skipped gradient); gating on a graph plan; argument errors.
+bases, a skipped gradient); the autograd wrapper cgconv_graph; gating on a
+graph plan; argument errors.
 """
 
 import numpy as np
@@ -157,3 +158,31 @@ def test_graph_backward(shape, orth):
     eq, ek = rel_l2(gq, rq), rel_l2(gk, rk)
     print(f"[parity] graph backward {shape} orthonormal={orth}: dq {eq:.3e} dk {ek:.3e}", flush=True)
     assert eq <= TOL and ek <= TOL and rel_l2(gk2, rk) <= TOL
+
+
+def test_graph_autograd_wrapper():
+    """cgconv_graph: torch autograd through the graph plan's forward and
+    backward, against the oracle's chain rule; U takes no gradient."""
+    torch = _torch()
+    import paper_2509_24093_amd as P
+    B, n, L, C = 2, 96, 3, 3
+    rng = np.random.default_rng(6500)
+    U = _orth(rng, B, n)
+    q, k = W.iid(B, n, L, C, seed=6501)
+    g = rng.normal(size=q.shape).astype(np.float32)
+    print(f"[gpu] cgconv_graph autograd B={B} N={n} L={L} C={C}", flush=True)
+    plan = P.GraphPlan(B, n, L, C)
+    tU = torch.from_numpy(U).cuda()
+    tq = torch.from_numpy(q).cuda().requires_grad_(True)
+    tk = torch.from_numpy(k).cuda().requires_grad_(True)
+    out = P.cgconv_graph(tU, tq, tk, plan)
+    out.backward(torch.from_numpy(g).cuda())
+    torch.cuda.synchronize()
+    assert rel_l2(out.detach().cpu().numpy(), gft_cgconv(U, q, k, L)) <= TOL
+    rq, rk = gft_backward(U, q, k, g, L)
+    eq, ek = rel_l2(tq.grad.cpu().numpy(), rq), rel_l2(tk.grad.cpu().numpy(), rk)
+    print(f"[parity] graph autograd: dq {eq:.3e} dk {ek:.3e}", flush=True)
+    assert eq <= TOL and ek <= TOL
+    with pytest.raises(ValueError):
+        P.cgconv_graph(tU.clone().requires_grad_(True), tq, tk, plan)
+    plan.close()
