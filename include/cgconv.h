@@ -66,6 +66,15 @@ enum cgconv_status {
  * for the channel-mixing weights when L_max <= 6 and C <= 32, and small
  * tables; cgconv_plan_info reports the total) and uploads the tables.
  * Synchronous.  Returns NULL on failure (see cgconv_last_error()).
+ *
+ * Environment switches, read when a plan is created (all results stay within
+ * the same accuracy; they exist for cross-checks and tests):
+ *   CGCONV_UNFUSED=1        the modular five-kernel pipeline instead of the
+ *                           fused middle kernel;
+ *   CGCONV_FORCE_GENERIC=1  the table-driven contraction kernel instead of the
+ *                           generated per-L_max bodies (modular pipeline);
+ *   CGCONV_TEST_FAIL_ALLOC=1  token plans return NULL with the message of a
+ *                           failed workspace allocation (tests of that path).
  */
 cgconv_plan_t cgconv_plan_create(int64_t batch, int64_t N, int32_t L_max, int64_t C);
 
