@@ -33,7 +33,7 @@
 // a*(-b) and keeps a negated copy of every input alive for the whole kernel.
 //
 // A second body per L, CgPathBody<L>, keeps the paths apart for the
-// channel-mixing kernel (see emit_path_body); a third, CgRealBody<L>, is the
+// channel-mixing kernel, in steps (see emit_path_body); a third, CgRealBody<L>, is the
 // token-wise real-basis product of the value tensor product (emit_real_body).
 //
 // Usage: gen_cg <output-dir> <LGEN>   (writes cg_body_L<L>.inc and cg_lgen.h)
@@ -324,86 +324,132 @@ void emit_body(FILE* f, int L, long* ops_out) {
 
 }  // namespace
 
-// Per-path body for the channel-mixing kernel (CgPathBody<L>::run): the
-// products of every path p = (l1, l2, J) are kept apart.  Pairs (l1, l2) are
-// taken in lexicographic order, so path indices follow the same (l1, l2, J)
-// order as the weights.  Inside a pair the outputs are produced by M, with
-// the products qa[l1,m1] * ka[l2,M-m1] (4 ops) shared by all J of the pair;
-// every value w_p[M] goes to st.put(slot, value) with slot = the position of
-// (J, M) among the pair's outputs (J ascending, then M = -J..J), zeros
-// included; st.begin_pair<p0, n_paths>() precedes the pair's first value and
-// st.end_pair<p0, Jmin, Jmax>() follows its last one.
-void emit_path_body(FILE* f, int L, long* ops_out) {
-  const int K = (L + 1) * (L + 1);
-  std::vector<Term> terms = contraction_terms(L);
-  std::map<std::array<int, 4>, std::vector<Term>> by_pair_M;  // (l1, l2, M, -) -> terms
-  for (const Term& t : terms) by_pair_M[{t.l1, t.l2, t.M, 0}].push_back(t);
-  long ops = 0;
-  int path = 0, max_slots = 0;
-  std::fprintf(f, "template <>\nstruct CgPathBody<%d> {\n  static constexpr int K = %d;\n", L, K);
-  std::fprintf(f, "  template <class Store>\n");
-  std::fprintf(f,
-               "  static __device__ __forceinline__ void run(const float2 (&qa)[%d], const float2 (&ka)[%d], "
-               "Store& st) {\n",
-               K, K);
+// Per-path body for the channel-mixing kernel: the products of every path
+// p = (l1, l2, J) are kept apart, and the work is cut into steps small enough
+// to double-buffer their staged values in LDS.  Pairs (l1, l2) are taken in
+// lexicographic order (path indices follow the (l1, l2, J) order of the
+// weights); a pair's degrees J are cut, from the top, into runs Ja..Jb of at
+// most kStepSlotBudget outputs (J, M).  A step evaluates, M by M, the
+// products qa[l1,m1] * ka[l2,M-m1] (4 ops, shared by the J of the step) and
+// the values w_p[M] of its paths, each handed to st.put<B>(slot, value)
+// with B = step parity and slot = the position of (J, M) among the step's
+// outputs (J ascending, then M = -J..J), zeros included; st.end_m() follows
+// each M and st.end_step() each step.  CgPathBody<L>::produce is that sequence;
+// CgPathBody<L>::consume is the matching sequence of
+// st.step<B, P0, Ja, Jb, P0n, NPn>() calls (the step's first path and degree
+// range, and the first path and path count of the next step, NPn = 0 after
+// the last), preceded by st.first<P0, NP>() for the first step's weights.
+// A step that splits a pair recomputes the products its degrees need.
+constexpr int kStepSlotBudget = 24;
+
+struct MixStep {
+  int l1, l2, Ja, Jb, P0;
+};
+
+std::vector<MixStep> mix_steps(int L) {
+  std::vector<MixStep> steps;
+  int path = 0;
   for (int l1 = 0; l1 <= L; ++l1)
     for (int l2 = 0; l2 <= L; ++l2) {
       const int Jmin = std::abs(l1 - l2), Jmax = std::min(l1 + l2, L);
       if (Jmin > Jmax) continue;
-      int slots = 0;
-      for (int J = Jmin; J <= Jmax; ++J) slots += 2 * J + 1;
-      max_slots = std::max(max_slots, slots);
-      std::fprintf(f, "    {  // pair l1=%d l2=%d: paths %d..%d (J = %d..%d)\n", l1, l2, path, path + Jmax - Jmin,
-                   Jmin, Jmax);
-      std::fprintf(f, "      st.template begin_pair<%d, %d>();\n", path, Jmax - Jmin + 1);
-      for (int M = -Jmax; M <= Jmax; ++M) {
-        auto it = by_pair_M.find({l1, l2, M, 0});
-        std::map<int, std::vector<const Term*>> by_m1;
-        if (it != by_pair_M.end())
-          for (const Term& t : it->second) by_m1[t.m1].push_back(&t);
-        std::fprintf(f, "    {  // M = %d\n", M);
-        std::set<int> inited;
-        for (int J = std::max(Jmin, std::abs(M)); J <= Jmax; ++J) std::fprintf(f, "      float2 t%d;\n", J);
-        for (auto& e : by_m1) {
-          const int m1 = e.first, m2 = M - m1;
-          const std::string q = qname(l1, m1), k = kname(l2, m2);
-          std::fprintf(f, "      { const float pr = fnma(%s.y, %s.y, %s.x * %s.x);", q.c_str(), k.c_str(), q.c_str(),
-                       k.c_str());
-          std::fprintf(f, " const float pi = fmaf(%s.y, %s.x, %s.x * %s.y);\n", q.c_str(), k.c_str(), q.c_str(),
-                       k.c_str());
-          ops += 4;
-          for (const Term* t : e.second) {
-            const std::string a = "t" + std::to_string(t->J);
-            const std::string re_src = t->imag ? "pi" : "pr", im_src = t->imag ? "pr" : "pi";
-            const double re_c = t->imag ? -t->coef : t->coef, im_c = t->coef;
-            if (!inited.count(t->J))
-              std::fprintf(f, "      %s.x = %s * %s; %s.y = %s * %s;\n", a.c_str(), lit(re_c).c_str(),
-                           re_src.c_str(), a.c_str(), lit(im_c).c_str(), im_src.c_str());
-            else
-              std::fprintf(f, "      %s.x = fmaf(%s, %s, %s.x); %s.y = fmaf(%s, %s, %s.y);\n", a.c_str(),
-                           lit(re_c).c_str(), re_src.c_str(), a.c_str(), a.c_str(), lit(im_c).c_str(),
-                           im_src.c_str(), a.c_str());
-            inited.insert(t->J);
-            ops += 2;
-          }
-          std::fprintf(f, "      }\n");
-        }
-        int base = 0;
-        for (int J = Jmin; J <= Jmax; ++J) {
-          if (std::abs(M) <= J) {
-            if (!inited.count(J)) std::fprintf(f, "      t%d = make_float2(0.f, 0.f);\n", J);
-            std::fprintf(f, "      st.put(%d, t%d);\n", base + M + J, J);
-          }
-          base += 2 * J + 1;
-        }
-        std::fprintf(f, "    }\n");
+      int J = Jmax;
+      while (J >= Jmin) {
+        const int Jb = J;
+        int slots = 2 * J + 1;
+        --J;
+        while (J >= Jmin && slots + 2 * J + 1 <= kStepSlotBudget) slots += 2 * J-- + 1;
+        steps.push_back({l1, l2, J + 1, Jb, path + (J + 1 - Jmin)});
       }
-      std::fprintf(f, "      st.template end_pair<%d, %d, %d>();\n    }\n", path, Jmin, Jmax);
       path += Jmax - Jmin + 1;
     }
+  return steps;
+}
+
+void emit_path_body(FILE* f, int L, long* ops_out) {
+  const int K = (L + 1) * (L + 1);
+  std::vector<Term> terms = contraction_terms(L);
+  std::map<std::array<int, 3>, std::vector<Term>> by_pair_M;  // (l1, l2, M) -> terms
+  for (const Term& t : terms) by_pair_M[{t.l1, t.l2, t.M}].push_back(t);
+  const std::vector<MixStep> steps = mix_steps(L);
+  long ops = 0;
+  int max_slots = 0, max_paths = 0, n_paths = 0;
+  for (const MixStep& st : steps) n_paths = std::max(n_paths, st.P0 + st.Jb - st.Ja + 1);
+  std::fprintf(f, "template <>\nstruct CgPathBody<%d> {\n  static constexpr int K = %d;\n", L, K);
+  std::fprintf(f, "  template <class Store>\n");
+  std::fprintf(f,
+               "  static __device__ __forceinline__ void produce(const float2 (&qa)[%d], const float2 (&ka)[%d], "
+               "Store& st) {\n",
+               K, K);
+  for (size_t si = 0; si < steps.size(); ++si) {
+    const MixStep& sp = steps[si];
+    const int B = (int)(si & 1);
+    int slots = 0;
+    for (int J = sp.Ja; J <= sp.Jb; ++J) slots += 2 * J + 1;
+    max_slots = std::max(max_slots, slots);
+    max_paths = std::max(max_paths, sp.Jb - sp.Ja + 1);
+    std::fprintf(f, "    {  // step %zu: pair l1=%d l2=%d, J = %d..%d (paths %d..%d)\n", si, sp.l1, sp.l2, sp.Ja, sp.Jb,
+                 sp.P0, sp.P0 + sp.Jb - sp.Ja);
+    for (int M = -sp.Jb; M <= sp.Jb; ++M) {
+      auto it = by_pair_M.find({sp.l1, sp.l2, M});
+      std::map<int, std::vector<const Term*>> by_m1;
+      if (it != by_pair_M.end())
+        for (const Term& t : it->second)
+          if (t.J >= sp.Ja && t.J <= sp.Jb) by_m1[t.m1].push_back(&t);
+      std::fprintf(f, "    {  // M = %d\n", M);
+      std::set<int> inited;
+      for (int J = std::max(sp.Ja, std::abs(M)); J <= sp.Jb; ++J) std::fprintf(f, "      float2 t%d;\n", J);
+      for (auto& e : by_m1) {
+        const int m1 = e.first, m2 = M - m1;
+        const std::string q = qname(sp.l1, m1), k = kname(sp.l2, m2);
+        std::fprintf(f, "      { const float pr = fnma(%s.y, %s.y, %s.x * %s.x);", q.c_str(), k.c_str(), q.c_str(),
+                     k.c_str());
+        std::fprintf(f, " const float pi = fmaf(%s.y, %s.x, %s.x * %s.y);\n", q.c_str(), k.c_str(), q.c_str(),
+                     k.c_str());
+        ops += 4;
+        for (const Term* t : e.second) {
+          const std::string a = "t" + std::to_string(t->J);
+          const std::string re_src = t->imag ? "pi" : "pr", im_src = t->imag ? "pr" : "pi";
+          const double re_c = t->imag ? -t->coef : t->coef, im_c = t->coef;
+          if (!inited.count(t->J))
+            std::fprintf(f, "      %s.x = %s * %s; %s.y = %s * %s;\n", a.c_str(), lit(re_c).c_str(),
+                         re_src.c_str(), a.c_str(), lit(im_c).c_str(), im_src.c_str());
+          else
+            std::fprintf(f, "      %s.x = fmaf(%s, %s, %s.x); %s.y = fmaf(%s, %s, %s.y);\n", a.c_str(),
+                         lit(re_c).c_str(), re_src.c_str(), a.c_str(), a.c_str(), lit(im_c).c_str(),
+                         im_src.c_str(), a.c_str());
+          inited.insert(t->J);
+          ops += 2;
+        }
+        std::fprintf(f, "      }\n");
+      }
+      int base = 0;
+      for (int J = sp.Ja; J <= sp.Jb; ++J) {
+        if (std::abs(M) <= J) {
+          if (!inited.count(J)) std::fprintf(f, "      t%d = make_float2(0.f, 0.f);\n", J);
+          std::fprintf(f, "      st.template put<%d>(%d, t%d);\n", B, base + M + J, J);
+        }
+        base += 2 * J + 1;
+      }
+      std::fprintf(f, "      st.end_m();\n    }\n");
+    }
+    std::fprintf(f, "      st.end_step();\n    }\n");
+  }
   std::fprintf(f, "  }\n");
-  std::fprintf(f, "  static constexpr int kPaths = %d;\n", path);
-  std::fprintf(f, "  static constexpr int kMaxPairSlots = %d;  // most outputs (J, M) of one pair\n", max_slots);
+  std::fprintf(f, "  template <class Store>\n  static __device__ __forceinline__ void consume(Store& st) {\n");
+  std::fprintf(f, "    st.template first<%d, %d>();\n", steps[0].P0, steps[0].Jb - steps[0].Ja + 1);
+  for (size_t si = 0; si < steps.size(); ++si) {
+    const MixStep& sp = steps[si];
+    const int P0n = si + 1 < steps.size() ? steps[si + 1].P0 : 0;
+    const int NPn = si + 1 < steps.size() ? steps[si + 1].Jb - steps[si + 1].Ja + 1 : 0;
+    std::fprintf(f, "    st.template step<%d, %d, %d, %d, %d, %d>();\n", (int)(si & 1), sp.P0, sp.Ja, sp.Jb, P0n,
+                 NPn);
+  }
+  std::fprintf(f, "  }\n");
+  std::fprintf(f, "  static constexpr int kPaths = %d;\n", n_paths);
+  std::fprintf(f, "  static constexpr int kSteps = %d;\n", (int)steps.size());
+  std::fprintf(f, "  static constexpr int kMaxStepSlots = %d;  // most outputs (J, M) of one step\n", max_slots);
+  std::fprintf(f, "  static constexpr int kMaxStepPaths = %d;  // most paths of one step\n", max_paths);
   std::fprintf(f, "  static constexpr long kOps = %ld;  // VALU ops of the per-path products per point\n};\n\n", ops);
   *ops_out = ops;
 }
