@@ -272,12 +272,20 @@ def test_fused_matches_modular_and_oracle(shape):
     assert err <= TOL_F32
 
 
-def test_fused_bf16():
-    q, k = W.iid(2, 2048, 6, 8, seed=77)
+@pytest.mark.parametrize("shape", [(2, 2048, 6, 8), (1, 32768, 4, 6), (1, 32768, 2, 5)],
+                         ids=lambda s: "B%dN%dL%dC%d" % s)
+def test_fused_bf16(shape):
+    """bf16 storage on the fused pipeline: radix-32 outer passes at N = 2048
+    (N1 = 32) and radix-512 ones at 32768, paired bf16 loads (even C) and
+    single ones (odd C)."""
+    B, N, L, C = shape
+    q, k = W.iid(B, N, L, C, seed=77 + N + C)
     qb, kb = W.to_bf16_bits(q), W.to_bf16_bits(k)
-    got = gpu_forward(qb, kb, 6, bf16=True, tag="fused bf16")
-    ref = cgconv_fft(W.bf16_bits_to_f32(qb), W.bf16_bits_to_f32(kb), 6)
-    assert rel_l2(got, ref) <= TOL_BF16
+    got = gpu_forward(qb, kb, L, bf16=True, tag="fused bf16 " + str(shape))
+    ref = cgconv_fft(W.bf16_bits_to_f32(qb), W.bf16_bits_to_f32(kb), L)
+    err = rel_l2(got, ref)
+    print(f"  fused bf16 {shape}: rel_l2 = {err:.3e}", flush=True)
+    assert err <= TOL_BF16
 
 
 @pytest.mark.parametrize("N,L,expect", [(256, 3, ["fft_fwd", "cg", "fft_inv"]),
