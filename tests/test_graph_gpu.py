@@ -186,3 +186,24 @@ def test_graph_autograd_wrapper():
     with pytest.raises(ValueError):
         P.cgconv_graph(tU.clone().requires_grad_(True), tq, tk, plan)
     plan.close()
+
+
+def test_graph_largest_plan():
+    """N = CGCONV_GRAPH_NMAX = 16384 nodes (2 GB of split bases per batch
+    element): an orthonormal basis built as a Sylvester Hadamard matrix
+    (entry (i, j) = (-1)^popcount(i & j)) with permuted rows and random column
+    signs, over sqrt(N); whole channels against the oracle."""
+    import paper_2509_24093_amd as P
+    n, L, C = P.CGCONV_GRAPH_NMAX, 2, 2
+    rng = np.random.default_rng(6600)
+    rows = rng.permutation(n).astype(np.uint16)
+    odd = (np.bitwise_count(np.bitwise_and.outer(rows, np.arange(n, dtype=np.uint16))) & np.uint8(1)).astype(bool)
+    sgn = (rng.choice([-1.0, 1.0], size=n) / np.sqrt(n)).astype(np.float32)
+    U = np.where(odd, -sgn, sgn)
+    del odd
+    q, k = W.iid(1, n, L, C, seed=6601)
+    got = gpu_graph(U[None], q, k, L, "largest")
+    ref = gft_cgconv(U[None], q, k, L)
+    err = rel_l2(got, ref)
+    print(f"[parity] graph N={n}: rel_l2 {err:.3e}", flush=True)
+    assert err <= TOL
