@@ -69,3 +69,37 @@ def value_tensor_product(a, v, L: int) -> np.ndarray:
 def gate_value(u, v, L: int) -> np.ndarray:
     """Algorithm 1 step 5 as read here: value_tensor_product(gate(u), v)."""
     return value_tensor_product(gate(u, L), v, L)
+
+
+def gate_value_backward(u, v, G, L: int):
+    """(du, dv) of a scalar loss with dL/df = G, for f = gate_value(u, v), by
+    the chain rule through the definitions above (float64):
+
+        a = g u (g broadcast over the 2l+1 components of each degree)
+        dv[y] = sum_{o,x} R[o,x,y] G[o] a[x]        da[x] = sum_{o,y} R[o,x,y] G[o] v[y]
+        dg[b,i,l,c] = sum_m u[(l,m)] da[(l,m)]       (the gate's own gradient)
+        dI[b,i,l,c] = g (dg - sum_j g[b,j,l,c] dg[b,j,l,c])   (softmax over the tokens)
+        du = g da + (dI / I) u                      (I = ||u_l||; no term where I = 0)
+    """
+    u = np.asarray(u, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    G = np.asarray(G, dtype=np.float64)
+    if not (u.shape == v.shape == G.shape) or u.ndim != 4 or u.shape[2] != n_comp(L):
+        raise ValueError("u, v and G must all have shape (B, N, (L+1)^2, C)")
+    reps = [2 * l + 1 for l in range(L + 1)]
+    I = invariant_norms(u, L)
+    g = softmax_tokens(I)
+    a = u * np.repeat(g, reps, axis=2)
+    R = dense_R(L)
+    dv = np.einsum("oxy,bioc,bixc->biyc", R, G, a, optimize=True)
+    da = np.einsum("oxy,bioc,biyc->bixc", R, G, v, optimize=True)
+    B, N, K, C = u.shape
+    dg = np.empty((B, N, L + 1, C))
+    for l in range(L + 1):
+        sl = slice(l * l, (l + 1) ** 2)
+        dg[:, :, l, :] = np.sum(u[:, :, sl, :] * da[:, :, sl, :], axis=2)
+    dI = g * (dg - np.sum(g * dg, axis=1, keepdims=True))
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(I > 0, dI / I, 0.0)
+    du = np.repeat(g, reps, axis=2) * da + np.repeat(ratio, reps, axis=2) * u
+    return du, dv
