@@ -226,6 +226,25 @@ int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const fl
 int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float* f, hipStream_t stream);
 
 /*
+ * Backward of cgconv_gate_value (the models of §5 are trained through this
+ * step too): given grad_f = dL/df, the gradients with respect to u and v by
+ * the chain rule through the definition above, with a = g u:
+ *
+ *   grad_v = R-transposed contraction of (grad_f, a), grad_a = that of (grad_f, v)
+ *   h[b,i,l,c] = g sum_m u grad_a                   (the gate's gradient times g)
+ *   grad_u = g grad_a + (h - g sum_j h[b,j,l,c]) u / I   (softmax and norm; no term where I = 0)
+ *
+ * Both contractions are forward token-wise products under the per-degree
+ * scales of cgconv_backward.  u, v, grad_f: DEVICE pointers, fp32, the layout
+ * of cgconv_gate_value; grad_u, grad_v: outputs of the same layout, either
+ * may be NULL (skipped), not both; they must not alias the inputs or each
+ * other.  Uses the plan's gating workspace (about 4 batch*N*(L_max+1)*C
+ * bytes more than the forward); same stream rules as cgconv_forward.
+ */
+int cgconv_gate_value_backward(cgconv_plan_t plan, const float* u, const float* v, const float* grad_f,
+                               float* grad_u, float* grad_v, hipStream_t stream);
+
+/*
  * Host-only (no GPU needed): the CG paths at L_max in the order the mixing
  * weights use, every triangle-allowed (l1, l2, J) with l1, l2, J <= L_max
  * (odd l1+l2+J included), lexicographic in (l1, l2, J).  Writes up to cap
@@ -282,7 +301,8 @@ int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, 
  * fixes which kind is timed: plain forwards, mixed forwards (cg_mix replaces
  * cg and the unfused passes are listed), backwards (each of the two
  * gradients is one timed call with the plain stages), gating calls
- * (gate_partials, gate_finalize, gate_value) or graph forwards
+ * (gate_partials, gate_finalize, gate_value), gating backwards (gate_stats,
+ * gate_bwd, gate_sums, gate_bwd_du) or graph forwards
  * (gft_split_u, gft_split_x, gft_gemm_fwd, gft_product, gft_split_uhat,
  * gft_gemm_inv); calls of the other kinds are not timed.
  * cgconv_plan_stage_name returns a stage's name ("" if out of range).

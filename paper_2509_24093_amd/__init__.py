@@ -69,6 +69,8 @@ def library() -> ctypes.CDLL:
     lib.cgconv_backward.restype = ctypes.c_int
     lib.cgconv_gate_value.argtypes = [vp, vp, vp, vp, vp]
     lib.cgconv_gate_value.restype = ctypes.c_int
+    lib.cgconv_gate_value_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    lib.cgconv_gate_value_backward.restype = ctypes.c_int
     lib.cgconv_paths.argtypes = [i32, ctypes.POINTER(i32), i64]
     lib.cgconv_paths.restype = i64
     lib.cgconv_plan_destroy.argtypes = [vp]
@@ -160,6 +162,12 @@ def cgconv_backward(plan: int, q: int, k: int, grad_out: int, grad_q, grad_k, st
 def cgconv_gate_value(plan: int, u: int, v: int, f: int, stream: int) -> int:
     """Invariant softmax gating of u and its token-wise CG product with v."""
     return _check(library().cgconv_gate_value(plan, u, v, f, stream))
+
+
+def cgconv_gate_value_backward(plan: int, u: int, v: int, grad_f: int, grad_u, grad_v, stream: int) -> int:
+    """Gradients of a scalar loss through cgconv_gate_value with respect to u
+    and v given grad_f (device pointers; grad_u or grad_v may be None)."""
+    return _check(library().cgconv_gate_value_backward(plan, u, v, grad_f, grad_u, grad_v, stream))
 
 
 def cgconv_paths(L_max: int):
@@ -300,6 +308,23 @@ class Plan:
         cgconv_gate_value(self._h, u.data_ptr(), v.data_ptr(), out.data_ptr(), s)
         return out
 
+    def gate_value_backward(self, u, v, grad_f, need_u: bool = True, need_v: bool = True):
+        """(grad_u, grad_v) of a scalar loss through gate_value given grad_f
+        (fp32); a gradient that is not needed is returned as None."""
+        import torch
+        if not (need_u or need_v):
+            return None, None
+        gu = torch.empty(self.shape, dtype=torch.float32, device=u.device) if need_u else None
+        gv = torch.empty(self.shape, dtype=torch.float32, device=u.device) if need_v else None
+        s = self._args(u, v, grad_f, torch.float32)
+        for t in (gu, gv):
+            if t is not None:
+                self._args(t, t, t, torch.float32)
+        cgconv_gate_value_backward(self._h, u.data_ptr(), v.data_ptr(), grad_f.data_ptr(),
+                                   gu.data_ptr() if gu is not None else None,
+                                   gv.data_ptr() if gv is not None else None, s)
+        return gu, gv
+
     def backward(self, q, k, grad_out, need_q: bool = True, need_k: bool = True):
         """(grad_q, grad_k) of a scalar loss given grad_out = dL/dout (fp32);
         a gradient that is not needed is returned as None."""
@@ -398,6 +423,35 @@ class GraphPlan(Plan):
         return gq, gk
 
     __call__ = forward
+
+
+_gate_fn = None
+
+
+def cgconv_gate(u, v, plan: Plan):
+    """Differentiable gating + value tensor product of fp32 tensors in u and
+    v: the forward and the backward are the plan's cgconv_gate_value and
+    cgconv_gate_value_backward."""
+    global _gate_fn
+    if _gate_fn is None:
+        import torch
+
+        class _GateFn(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, u, v, plan):
+                ctx.save_for_backward(u, v)
+                ctx.plan = plan
+                return plan.gate_value(u, v)
+
+            @staticmethod
+            def backward(ctx, grad_f):
+                u, v = ctx.saved_tensors
+                gu, gv = ctx.plan.gate_value_backward(u, v, grad_f.contiguous(), need_u=ctx.needs_input_grad[0],
+                                                      need_v=ctx.needs_input_grad[1])
+                return gu, gv, None
+
+        _gate_fn = _GateFn
+    return _gate_fn.apply(u, v, plan)
 
 
 _graph_fn = None

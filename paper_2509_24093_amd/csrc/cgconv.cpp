@@ -28,6 +28,7 @@
 
 #include "cgconv.h"
 #include "cg_table.h"
+#include "gate_bwd.h"
 #include "gft.h"
 #include "kernels.h"
 
@@ -83,6 +84,8 @@ struct cgconv_plan {
   uint16_t* d_wmix = nullptr;  // channel-mixing weights, split bf16 MFMA operands (L <= 6, C <= 32)
   float2* d_gpart = nullptr;   // gating: online-softmax partials per token chunk
   float2* d_gfin = nullptr;    // gating: maximum and denominator per (b, l, c)
+  float* d_gh = nullptr;       // gating backward: h per (b, i, l, c)
+  float* d_gS = nullptr;       // gating backward: sum of h over the tokens per (b, l, c)
   float* d_bscale = nullptr;   // backward: per-component scales, [2 gradients][in a, in b, out][K]
   bool force_generic = false;
   // optional per-stage timing: events recorded on the forward's stream.  The
@@ -108,6 +111,8 @@ void free_plan(cgconv_plan* p) {
   (void)hipFree(p->d_wmix);
   (void)hipFree(p->d_gpart);
   (void)hipFree(p->d_gfin);
+  (void)hipFree(p->d_gh);
+  (void)hipFree(p->d_gS);
   (void)hipFree(p->d_bscale);
   (void)hipFree(p->g_block);
   for (hipEvent_t ev : p->events) (void)hipEventDestroy(ev);
@@ -121,10 +126,13 @@ const char* const kStagesF[] = {"fft_fwd_1", "cg_fused", "fft_inv_2"};
 const char* const kStagesM2[] = {"fft_fwd_1", "fft_fwd_2", "cg_mix", "fft_inv_1", "fft_inv_2"};
 const char* const kStagesM1[] = {"fft_fwd", "cg_mix", "fft_inv"};
 const char* const kStagesG[] = {"gate_partials", "gate_finalize", "gate_value"};
+const char* const kStagesGB[] = {"gate_stats", "gate_bwd", "gate_sums", "gate_bwd_du"};
 const char* const kStagesGft[] = {"gft_split_u", "gft_split_x", "gft_gemm_fwd", "gft_product", "gft_split_uhat",
                                   "gft_gemm_inv"};
-// timing kinds: 0 forward, 1 mixed forward, 2 backward (each gradient one call), 3 gating, 4 graph forward
+// timing kinds: 0 forward, 1 mixed forward, 2 backward (each gradient one call), 3 gating, 4 graph forward,
+// 5 gating backward
 constexpr int kKindGate = 3;
+constexpr int kKindGateBwd = 5;
 constexpr int kKindGraph = 4;
 constexpr int kMaxEvents = 8;  // stages + 1 of the longest pipeline
 
@@ -154,6 +162,21 @@ hipError_t launch_gate(int L, const GateArgs& a, hipStream_t s) {
     case 6: return launch_gate_value<6>(a, s);
     case 7: return launch_gate_value<7>(a, s);
     case 8: return launch_gate_value<8>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gate_bwd(int L, const GateBwdArgs& a, hipStream_t s) {
+  switch (L) {
+    case 0: return launch_gate_backward<0>(a, s);
+    case 1: return launch_gate_backward<1>(a, s);
+    case 2: return launch_gate_backward<2>(a, s);
+    case 3: return launch_gate_backward<3>(a, s);
+    case 4: return launch_gate_backward<4>(a, s);
+    case 5: return launch_gate_backward<5>(a, s);
+    case 6: return launch_gate_backward<6>(a, s);
+    case 7: return launch_gate_backward<7>(a, s);
+    case 8: return launch_gate_backward<8>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -410,7 +433,10 @@ hipError_t alloc_gate_workspace(cgconv_plan* p) {
   hipError_t e;
   if ((e = hipMalloc(&p->d_gpart, np * sizeof(float2))) != hipSuccess) return e;
   if ((e = hipMalloc(&p->d_gfin, nf * sizeof(float2))) != hipSuccess) return e;
-  p->ws_bytes += (np + nf) * sizeof(float2);
+  const size_t nh = (size_t)p->B * p->Nu * (p->L + 1) * p->C;
+  if ((e = hipMalloc(&p->d_gh, nh * sizeof(float))) != hipSuccess) return e;
+  if ((e = hipMalloc(&p->d_gS, nf * sizeof(float))) != hipSuccess) return e;
+  p->ws_bytes += (np + nf) * sizeof(float2) + (nh + nf) * sizeof(float);
   return hipSuccess;
 }
 
@@ -898,6 +924,7 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
   }
   const int ns = plan->timing_kind == 1           ? plan->n_stages_mix
                  : plan->timing_kind == kKindGate  ? 3
+                 : plan->timing_kind == kKindGateBwd ? 4
                  : plan->timing_kind == kKindGraph ? 6
                                                    : plan->n_stages;
   if (n_stages) *n_stages = ns;
@@ -930,6 +957,7 @@ const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
     return plan->N1 ? kStagesM2[stage] : kStagesM1[stage];
   }
   if (plan->timing_kind == kKindGate) return stage < 3 ? kStagesG[stage] : "";
+  if (plan->timing_kind == kKindGateBwd) return stage < 4 ? kStagesGB[stage] : "";
   if (plan->timing_kind == kKindGraph) return stage < 6 ? kStagesGft[stage] : "";
   if (stage >= plan->n_stages) return "";
   if (plan->fused) return kStagesF[stage];
@@ -1033,6 +1061,67 @@ int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float*
     ++plan->timing_calls;
   }
   const hipError_t e = launch_gate(plan->L, a, stream);
+  if (e != hipSuccess) {
+    set_error("kernel launch failed: %s", hipGetErrorString(e));
+    return CGCONV_ERR_HIP;
+  }
+  return CGCONV_OK;
+}
+
+int cgconv_gate_value_backward(cgconv_plan_t plan, const float* u, const float* v, const float* grad_f,
+                               float* grad_u, float* grad_v, hipStream_t stream) {
+  if (!plan) {
+    set_error("plan is NULL");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!u || !v || !grad_f || (!grad_u && !grad_v)) {
+    set_error("u, v and grad_f must be non-NULL, and at least one of grad_u, grad_v");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const void* ptrs[] = {u, v, grad_f, grad_u, grad_v};
+  for (const void* ptr : ptrs) {
+    if (ptr && !aligned16(ptr)) {
+      set_error("u, v, grad_f, grad_u and grad_v must be 16-byte aligned");
+      return CGCONV_ERR_ALIGNMENT;
+    }
+  }
+  for (const float* g : {grad_u, grad_v}) {
+    if (g && (g == u || g == v || g == grad_f)) {
+      set_error("grad_u and grad_v must not alias u, v or grad_f");
+      return CGCONV_ERR_INVALID_ARG;
+    }
+  }
+  if (grad_u && grad_u == grad_v) {
+    set_error("grad_u and grad_v must be distinct");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) {
+    set_error("the plan's device (%d) is not current (%d)", plan->device, cur);
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  GateBwdArgs a;
+  a.u = u;
+  a.v = v;
+  a.G = grad_f;
+  a.du = grad_u;
+  a.dv = grad_v;
+  a.h = plan->d_gh;
+  a.psum = reinterpret_cast<float*>(plan->d_gpart);  // free once the softmax statistics are formed
+  a.S = plan->d_gS;
+  a.part = plan->d_gpart;
+  a.fin = plan->d_gfin;
+  a.scales = plan->d_bscale;
+  a.B = (int)plan->B;
+  a.N = (int)plan->Nu;
+  a.C = (int)plan->C;
+  a.events = nullptr;
+  if (plan->timing_calls < plan->timing_max && (plan->timing_kind < 0 || plan->timing_kind == kKindGateBwd)) {
+    plan->timing_kind = kKindGateBwd;
+    a.events = &plan->events[(size_t)plan->timing_calls * kMaxEvents];
+    ++plan->timing_calls;
+  }
+  const hipError_t e = launch_gate_bwd(plan->L, a, stream);
   if (e != hipSuccess) {
     set_error("kernel launch failed: %s", hipGetErrorString(e));
     return CGCONV_ERR_HIP;

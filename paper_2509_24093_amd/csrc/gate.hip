@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include "cg_common.h"
+#include "gate_bwd.h"
 #include "gft.h"
 
 namespace cgconv {
@@ -176,6 +177,150 @@ __global__ __launch_bounds__(kGateThreads) void gate_value_kernel(const float* _
   for (int k = 0; k < K; ++k) z[(long long)k * C] = out[k];
 }
 
+// Backward, one lane per (b, i, c): the gradients of the token-wise product
+// with respect to its two operands are forward products of the output
+// gradient under per-degree scales (the transposition identity of the
+// real-basis tensor, as for the convolution's backward):
+//   da = s_o .* TP(s_a .* G, s_b .* v)   (first-operand scales, scales[0..3K))
+//   dv = t_o .* TP(t_a .* G, a)          (second-operand scales, scales[3K..6K), t_b = 1)
+// with a = g u.  The lane stores dv, du = g da (the gate held fixed) and
+// h[l] = g[l] sum_m u[l,m] da[l,m] for the softmax and norm terms.
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gate_bwd_kernel(GateBwdArgs a, long long lanes) {
+  constexpr int K = (L + 1) * (L + 1);
+  const long long p = (long long)blockIdx.x * kGateThreads + threadIdx.x;
+  if (p >= lanes) return;
+  const int c = (int)(p % a.C);
+  const long long bi = p / a.C;  // b * N + i
+  const long long b = bi / a.N;
+  const long long base = bi * K * a.C + c;
+  float x[K], gr[K], w[K], out[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    x[k] = a.u[base + (long long)k * a.C];
+    gr[k] = a.G[base + (long long)k * a.C] * a.scales[k];
+    w[k] = a.v[base + (long long)k * a.C] * a.scales[K + k];
+  }
+  float I[L + 1], g[L + 1];
+  degree_norms<L>(x, I);
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
+    const float2 ms = a.fin[(b * (L + 1) + l) * a.C + c];
+    g[l] = __expf(I[l] - ms.x) / ms.y;
+#pragma unroll
+    for (int m = 0; m < 2 * l + 1; ++m) x[l * l + m] *= g[l];  // x = a = g u
+  }
+  if (a.du) {  // uniform
+    CgRealBody<L>::run(gr, w, out);  // out = da / s_o
+#pragma unroll
+    for (int l = 0; l <= L; ++l) {
+      float s = 0.f;
+#pragma unroll
+      for (int m = 0; m < 2 * l + 1; ++m) {
+        const int k = l * l + m;
+        const float da = out[k] * a.scales[2 * K + k];
+        s = fmaf(x[k], da, s);  // g sum_m u da = sum_m a da
+        a.du[base + (long long)k * a.C] = g[l] * da;
+      }
+      a.h[(bi * (L + 1) + l) * a.C + c] = s;
+    }
+  }
+  if (a.dv) {  // uniform
+#pragma unroll
+    for (int k = 0; k < K; ++k) gr[k] *= a.scales[3 * K + k] / a.scales[k];  // first-operand to second-operand scale
+    CgRealBody<L>::run(gr, x, out);
+#pragma unroll
+    for (int k = 0; k < K; ++k) a.dv[base + (long long)k * a.C] = out[k] * a.scales[5 * K + k];
+  }
+}
+
+// Sums of h over chunks of kGateChunk tokens, per (b, chunk, l, c): block
+// (chunk, b, channel group) with threads (token slot, channel) as in
+// gate_partials_kernel.
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gate_sum_partials_kernel(const float* __restrict__ h,
+                                                                         float* __restrict__ psum, int N, int C,
+                                                                         int chunks) {
+  __shared__ float red[kGateThreads][L + 1];
+  const int cpb = C < kGateThreads ? C : kGateThreads;
+  const int TS = kGateThreads / cpb;
+  const int tid = threadIdx.x;
+  const int c = blockIdx.z * cpb + tid % cpb, ts = tid / cpb;
+  const bool active = ts < TS && c < C && tid < TS * cpb;
+  const int chunk = blockIdx.x, b = blockIdx.y;
+  float acc[L + 1];
+#pragma unroll
+  for (int l = 0; l <= L; ++l) acc[l] = 0.f;
+  if (active) {
+    const int i_end = min(N, (chunk + 1) * kGateChunk);
+    for (int i = chunk * kGateChunk + ts; i < i_end; i += TS) {
+      const float* x = h + ((long long)b * N + i) * (L + 1) * C + c;
+#pragma unroll
+      for (int l = 0; l <= L; ++l) acc[l] += x[(long long)l * C];
+    }
+  }
+#pragma unroll
+  for (int l = 0; l <= L; ++l) red[tid][l] = acc[l];
+  __syncthreads();
+  if (active && ts == 0) {
+#pragma unroll
+    for (int l = 0; l <= L; ++l) {
+      float s = 0.f;
+      for (int t = 0; t < TS; ++t) s += red[t * cpb + tid % cpb][l];
+      psum[(((long long)b * chunks + chunk) * (L + 1) + l) * C + c] = s;
+    }
+  }
+}
+
+// One wave per (b, l, c): S = the sum of the chunk sums (lanes take chunks
+// lane, lane + 64, ..., then a shuffle tree).
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gate_sum_finalize_kernel(const float* __restrict__ psum,
+                                                                         float* __restrict__ S, int B, int C,
+                                                                         int chunks) {
+  const long long t = (long long)blockIdx.x * (kGateThreads / kWave) + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (t >= (long long)B * (L + 1) * C) return;  // whole wave
+  const int c = (int)(t % C);
+  const int l = (int)((t / C) % (L + 1));
+  const long long b = t / ((long long)C * (L + 1));
+  float s = 0.f;
+  for (int k = lane; k < chunks; k += kWave) s += psum[((b * chunks + k) * (L + 1) + l) * C + c];
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, kWave);
+  if (lane == 0) S[t] = s;  // [b][l][c]
+}
+
+// du += (dI / I) u with dI = g (dg - S') = h - g S per degree (the softmax
+// over the tokens and the norm); no term where I = 0.
+template <int L>
+__global__ __launch_bounds__(kGateThreads) void gate_bwd_du_kernel(GateBwdArgs a, long long lanes) {
+  constexpr int K = (L + 1) * (L + 1);
+  const long long p = (long long)blockIdx.x * kGateThreads + threadIdx.x;
+  if (p >= lanes) return;
+  const int c = (int)(p % a.C);
+  const long long bi = p / a.C;
+  const long long b = bi / a.N;
+  const long long base = bi * K * a.C + c;
+  float x[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) x[k] = a.u[base + (long long)k * a.C];
+  float I[L + 1];
+  degree_norms<L>(x, I);
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
+    const float2 ms = a.fin[(b * (L + 1) + l) * a.C + c];
+    const float g = __expf(I[l] - ms.x) / ms.y;
+    const float dI = a.h[(bi * (L + 1) + l) * a.C + c] - g * a.S[(b * (L + 1) + l) * a.C + c];
+    const float r = I[l] > 0.f ? dI / I[l] : 0.f;
+#pragma unroll
+    for (int m = 0; m < 2 * l + 1; ++m) {
+      const long long o = base + (long long)(l * l + m) * a.C;
+      a.du[o] = fmaf(r, x[l * l + m], a.du[o]);
+    }
+  }
+}
+
 // One lane per (b, f, c), c fastest: the CG product of the graph transforms.
 template <int L>
 __global__ __launch_bounds__(kGateThreads) void gft_product_kernel(GftProductArgs a, long long lanes) {
@@ -218,6 +363,51 @@ hipError_t launch_gft_product<CGCONV_TU_L>(const GftProductArgs& a, hipStream_t 
   hipLaunchKernelGGL(gft_product_kernel<CGCONV_TU_L>, dim3((unsigned)((lanes + kGateThreads - 1) / kGateThreads)),
                      dim3(kGateThreads), 0, s, a, lanes);
   return hipGetLastError();
+}
+
+template <>
+hipError_t launch_gate_backward<CGCONV_TU_L>(const GateBwdArgs& a, hipStream_t s) {
+  if (a.B < 1 || a.N < 1 || a.C < 1 || !a.u || !a.v || !a.G || (!a.du && !a.dv) || !a.part || !a.fin ||
+      !a.scales || (a.du && (!a.h || !a.psum || !a.S)))
+    return hipErrorInvalidValue;
+  const int chunks = (a.N + kGateChunk - 1) / kGateChunk;
+  const int cpb = a.C < kGateThreads ? a.C : kGateThreads;
+  const dim3 g1(chunks, a.B, (a.C + cpb - 1) / cpb);
+  const long long nf = (long long)a.B * (CGCONV_TU_L + 1) * a.C;  // one wave each
+  constexpr int wpb = kGateThreads / kWave;
+  const long long lanes = (long long)a.B * a.N * a.C;
+  const dim3 gl((unsigned)((lanes + kGateThreads - 1) / kGateThreads));
+  auto mark = [&](int i) {
+    if (a.events) (void)hipEventRecord(a.events[i], s);
+  };
+  mark(0);
+  // the forward's softmax statistics
+  hipLaunchKernelGGL(gate_partials_kernel<CGCONV_TU_L>, g1, dim3(kGateThreads), 0, s, a.u, a.part, a.N, a.C,
+                     chunks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(gate_finalize_kernel<CGCONV_TU_L>, dim3((unsigned)((nf + wpb - 1) / wpb)), dim3(kGateThreads), 0,
+                     s, a.part, a.fin, a.B, a.C, chunks);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  mark(1);
+  hipLaunchKernelGGL(gate_bwd_kernel<CGCONV_TU_L>, gl, dim3(kGateThreads), 0, s, a, lanes);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  mark(2);
+  if (a.du) {
+    hipLaunchKernelGGL(gate_sum_partials_kernel<CGCONV_TU_L>, g1, dim3(kGateThreads), 0, s, a.h, a.psum, a.N, a.C,
+                       chunks);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(gate_sum_finalize_kernel<CGCONV_TU_L>, dim3((unsigned)((nf + wpb - 1) / wpb)),
+                       dim3(kGateThreads), 0, s, a.psum, a.S, a.B, a.C, chunks);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  mark(3);
+  if (a.du) {
+    hipLaunchKernelGGL(gate_bwd_du_kernel<CGCONV_TU_L>, gl, dim3(kGateThreads), 0, s, a, lanes);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  mark(4);
+  return hipSuccess;
 }
 
 template <>
