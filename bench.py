@@ -27,7 +27,8 @@ random weights: its own JSON line, the mixing stage against the bf16 matrix
 core peak), --backward (cgconv_backward, both gradients, for a seeded
 output gradient: its own JSON line), --gate (cgconv_gate_value with the
 workload's q and k as u and v: its own JSON line, gate_value against the
-fp32 vector peak), --graph (cgconv_forward_graph on the graph workload,
+fp32 vector peak), --gate-backward (cgconv_gate_value_backward, both
+gradients, for a seeded upstream gradient: its own JSON line), --graph (cgconv_forward_graph on the graph workload,
 B=4, N=4096, L=6, C=32, with Laplacian eigenbases: its own JSON line, the
 forward transform against the bf16 matrix core peak), --boundary linear (any mode on a plan with the
 zero-padded token boundary: DFTs of length 2N).
@@ -57,6 +58,8 @@ METRIC_GRAPH = "CG-conv in a graph Fourier basis, tokens/sec at N=4096, L_max=6,
 METRIC_LINEAR = "CG-conv with the zero-padded (linear) boundary, tokens/sec at N=16384, L_max=6, C=32"
 METRIC_BACKWARD = "CG-conv backward (grad_q and grad_k), tokens/sec at N=16384, L_max=6, C=32"
 METRIC_GATE = "invariant softmax gating + value tensor product, tokens/sec at N=16384, L_max=6, C=32"
+METRIC_GATE_BACKWARD = ("gating + value tensor product backward (grad_u and grad_v), tokens/sec at N=16384, "
+                        "L_max=6, C=32")
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
 CG_SOURCES = ["paper_2509_24093_amd/csrc/cg_gen.hip", "paper_2509_24093_amd/csrc/cg_fused.hip",
               "paper_2509_24093_amd/csrc/cg_common.h", "paper_2509_24093_amd/csrc/fft_reg.h",
@@ -275,6 +278,7 @@ def main():
     ap.add_argument("--mixed", action="store_true")
     ap.add_argument("--backward", action="store_true")
     ap.add_argument("--gate", action="store_true")
+    ap.add_argument("--gate-backward", action="store_true")
     ap.add_argument("--boundary", choices=["cyclic", "linear"], default="cyclic")
     ap.add_argument("--graph", action="store_true")
     args = ap.parse_args()
@@ -323,6 +327,9 @@ def main():
         return
     if args.gate:
         bench_gate(args, plan, q, k, qd, kd, out, B, N, L, C)
+        return
+    if args.gate_backward:
+        bench_gate_backward(args, plan, q, k, qd, kd, B, N, L, C)
         return
     n_paths, nnz, n_products, ws_bytes = plan.info()
     log(f"[bench] plan: paths={n_paths} nnz={nnz} products={n_products} workspace={ws_bytes / 2**30:.2f} GiB")
@@ -647,6 +654,81 @@ def bench_gate(args, plan, q, k, qd, kd, out, B, N, L, C):
                                             f"({tokens:.0f} token-equivalents), fp64 numpy, {dt:.1f} s"}
         result["parity_rel_l2_sampled_channels"] = (num / den) ** 0.5
         log(f"[bench] gating parity on {len(chans)} channels: rel_l2 = {result['parity_rel_l2_sampled_channels']:.3e}")
+    else:
+        result["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(result), flush=True)
+
+
+def bench_gate_backward(args, plan, q, k, qd, kd, B, N, L, C):
+    """cgconv_gate_value_backward (grad_u and grad_v) with u = q, v = k of
+    the workload and a seeded upstream gradient ~ N(0, 1)."""
+    import numpy as np
+    import torch
+
+    import paper_2509_24093_amd as P
+    g = np.random.default_rng(2029).normal(size=q.shape).astype(np.float32)
+    gd = torch.from_numpy(g).cuda()
+    gu, gv = torch.empty_like(qd), torch.empty_like(qd)
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step():
+        P.cgconv_gate_value_backward(plan._h, qd.data_ptr(), kd.data_ptr(), gd.data_ptr(), gu.data_ptr(),
+                                     gv.data_ptr(), stream)
+    log(f"[bench] timing {args.steps} gating backward steps")
+    ms, stage_avg = _timed(args, step, plan)
+    K = (L + 1) ** 2
+    _, coef = P.cgconv_cg_table(L)
+    nnz_real = len(coef)
+    lanes = B * N * C
+    per_lane = 2 * (K * K + 2 * nnz_real) + 8 * K
+    flops = per_lane * lanes
+    bw_ms = stage_avg["gate_bwd"]
+    achieved = flops / (bw_ms * 1e-3) / 1e12
+    result = _common(args, METRIC_GATE_BACKWARD, ms, B, N, L, C, "f32")
+    result["roofline"] = {
+        "kernel": f"gate_bwd_kernel<{L}, false> + gate_bwd_kernel<{L}, true> (one launch per gradient)",
+        "bound": "alu",
+        "achieved": round(achieved, 2),
+        "peak": round(VALU_PEAK_TFLOPS, 1),
+        "unit": "TFLOP/s",
+        "frac": round(achieved / VALU_PEAK_TFLOPS, 4),
+        "traffic": None,
+        "flops_per_launch": flops,
+        "flop_model": (f"per (b, i, c) lane: two real-basis tensor products (one per gradient), each {K}^2 "
+                       f"products + 2 flops per non-zero ({nnz_real}), + 8K for the scales, the gate and "
+                       f"its sums; {lanes} lanes"),
+        "algorithmic_bytes_per_launch": 5 * K * 4 * lanes,
+        "achieved_gbs": round(5 * K * 4 * lanes / (bw_ms * 1e-3) / 1e9, 1),
+        "launch_ms": round(bw_ms, 4),
+    }
+    result["stages"] = {s: {"ms": round(t, 4)} for s, t in stage_avg.items()}
+    if not args.no_cpu_baseline:
+        from oracle.gate import gate_value_backward
+        log(f"[bench] CPU oracle baseline, gating backward (~{args.cpu_seconds:.0f} s)")
+        got = {"u": gu.cpu().numpy(), "v": gv.cpu().numpy()}
+        num = den = 0.0
+        chans = []
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_seconds and len(chans) < C:
+            c = len(chans)
+            sl = (slice(0, 1), slice(None), slice(None), slice(c, c + 1))
+            ru, rv = gate_value_backward(q[sl], k[sl], g[sl], L)
+            for name, ref in (("u", ru), ("v", rv)):
+                d = got[name][sl].astype(np.float64) - ref
+                num += float((d * d).sum())
+                den += float((ref * ref).sum())
+            chans.append(c)
+        dt = time.perf_counter() - t0
+        tokens = N * len(chans) / C
+        result["cpu_baseline"] = {"value": tokens / dt, "unit": "tokens/s", "cores": len(os.sched_getaffinity(0)),
+                                  "kind": "oracle",
+                                  "sample": f"both gradients, batch element 0, all {N} tokens, channels "
+                                            f"0..{len(chans) - 1} of {C} ({tokens:.0f} token-equivalents), "
+                                            f"fp64 numpy, {dt:.1f} s"}
+        result["parity_rel_l2_sampled_channels"] = (num / den) ** 0.5
+        log(f"[bench] gating backward parity on {len(chans)} channels: "
+            f"rel_l2 = {result['parity_rel_l2_sampled_channels']:.3e}")
     else:
         result["cpu_baseline"] = None
     plan.close()

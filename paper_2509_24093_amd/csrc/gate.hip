@@ -183,9 +183,13 @@ __global__ __launch_bounds__(kGateThreads) void gate_value_kernel(const float* _
 // real-basis tensor, as for the convolution's backward):
 //   da = s_o .* TP(s_a .* G, s_b .* v)   (first-operand scales, scales[0..3K))
 //   dv = t_o .* TP(t_a .* G, a)          (second-operand scales, scales[3K..6K), t_b = 1)
-// with a = g u.  The lane stores dv, du = g da (the gate held fixed) and
-// h[l] = g[l] sum_m u[l,m] da[l,m] for the softmax and norm terms.
-template <int L>
+// with a = g u.  DU = false stores dv; DU = true stores du = g da (the gate
+// held fixed) and h[l] = g[l] sum_m u[l,m] da[l,m] for the softmax and norm
+// terms.  The two gradients are separate launches so that each holds only
+// one product's operands and result in registers (3 waves per SIMD at
+// L_max = 6); u is read again for h after the product instead of being held
+// across it.
+template <int L, bool DU>
 __global__ __launch_bounds__(kGateThreads) void gate_bwd_kernel(GateBwdArgs a, long long lanes) {
   constexpr int K = (L + 1) * (L + 1);
   const long long p = (long long)blockIdx.x * kGateThreads + threadIdx.x;
@@ -194,43 +198,55 @@ __global__ __launch_bounds__(kGateThreads) void gate_bwd_kernel(GateBwdArgs a, l
   const long long bi = p / a.C;  // b * N + i
   const long long b = bi / a.N;
   const long long base = bi * K * a.C + c;
-  float x[K], gr[K], w[K], out[K];
+  float x[K], gr[K], out[K];
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    x[k] = a.u[base + (long long)k * a.C];
-    gr[k] = a.G[base + (long long)k * a.C] * a.scales[k];
-    w[k] = a.v[base + (long long)k * a.C] * a.scales[K + k];
-  }
+  for (int k = 0; k < K; ++k) x[k] = a.u[base + (long long)k * a.C];
   float I[L + 1], g[L + 1];
   degree_norms<L>(x, I);
 #pragma unroll
   for (int l = 0; l <= L; ++l) {
     const float2 ms = a.fin[(b * (L + 1) + l) * a.C + c];
     g[l] = __expf(I[l] - ms.x) / ms.y;
-#pragma unroll
-    for (int m = 0; m < 2 * l + 1; ++m) x[l * l + m] *= g[l];  // x = a = g u
   }
-  if (a.du) {  // uniform
-    CgRealBody<L>::run(gr, w, out);  // out = da / s_o
+  if (!DU) {
 #pragma unroll
     for (int l = 0; l <= L; ++l) {
-      float s = 0.f;
 #pragma unroll
-      for (int m = 0; m < 2 * l + 1; ++m) {
-        const int k = l * l + m;
-        const float da = out[k] * a.scales[2 * K + k];
-        s = fmaf(x[k], da, s);  // g sum_m u da = sum_m a da
-        a.du[base + (long long)k * a.C] = g[l] * da;
-      }
-      a.h[(bi * (L + 1) + l) * a.C + c] = s;
+      for (int m = 0; m < 2 * l + 1; ++m) x[l * l + m] *= g[l];  // x = a = g u
     }
-  }
-  if (a.dv) {  // uniform
 #pragma unroll
-    for (int k = 0; k < K; ++k) gr[k] *= a.scales[3 * K + k] / a.scales[k];  // first-operand to second-operand scale
+    for (int k = 0; k < K; ++k) gr[k] = a.G[base + (long long)k * a.C] * a.scales[3 * K + k];
     CgRealBody<L>::run(gr, x, out);
 #pragma unroll
     for (int k = 0; k < K; ++k) a.dv[base + (long long)k * a.C] = out[k] * a.scales[5 * K + k];
+    return;
+  }
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    gr[k] = a.G[base + (long long)k * a.C] * a.scales[k];
+    x[k] = a.v[base + (long long)k * a.C] * a.scales[K + k];  // x now holds v
+  }
+  CgRealBody<L>::run(gr, x, out);  // out = da / s_o
+  // An opaque copy of the lane offset: the addresses below are computed
+  // afresh instead of being shared with the first loads of u and held in
+  // registers across the product.
+  // All of u is read before the first store of du (which the compiler must
+  // assume may alias it), so the reads are not serialised behind the stores.
+  long long tail = base;
+  __asm__ volatile("" : "+v"(tail));
+#pragma unroll
+  for (int k = 0; k < K; ++k) x[k] = a.u[tail + (long long)k * a.C];
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
+    float s = 0.f;
+#pragma unroll
+    for (int m = 0; m < 2 * l + 1; ++m) {
+      const int k = l * l + m;
+      const float da = out[k] * a.scales[2 * K + k];
+      s = fmaf(x[k], da, s);
+      a.du[tail + (long long)k * a.C] = g[l] * da;
+    }
+    a.h[(bi * (L + 1) + l) * a.C + c] = g[l] * s;  // g sum_m u da
   }
 }
 
@@ -302,9 +318,15 @@ __global__ __launch_bounds__(kGateThreads) void gate_bwd_du_kernel(GateBwdArgs a
   const long long bi = p / a.C;
   const long long b = bi / a.N;
   const long long base = bi * K * a.C + c;
-  float x[K];
+  // Every read comes before the first store (du may alias the other
+  // operands as far as the compiler knows), so the reads are not serialised
+  // behind the stores.
+  float x[K], d[K], r[L + 1];
 #pragma unroll
-  for (int k = 0; k < K; ++k) x[k] = a.u[base + (long long)k * a.C];
+  for (int k = 0; k < K; ++k) {
+    x[k] = a.u[base + (long long)k * a.C];
+    d[k] = a.du[base + (long long)k * a.C];
+  }
   float I[L + 1];
   degree_norms<L>(x, I);
 #pragma unroll
@@ -312,11 +334,16 @@ __global__ __launch_bounds__(kGateThreads) void gate_bwd_du_kernel(GateBwdArgs a
     const float2 ms = a.fin[(b * (L + 1) + l) * a.C + c];
     const float g = __expf(I[l] - ms.x) / ms.y;
     const float dI = a.h[(bi * (L + 1) + l) * a.C + c] - g * a.S[(b * (L + 1) + l) * a.C + c];
-    const float r = I[l] > 0.f ? dI / I[l] : 0.f;
+    r[l] = I[l] > 0.f ? dI / I[l] : 0.f;
+  }
+  long long st = base;  // opaque copy: store addresses are not held from the loads
+  __asm__ volatile("" : "+v"(st));
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
 #pragma unroll
     for (int m = 0; m < 2 * l + 1; ++m) {
-      const long long o = base + (long long)(l * l + m) * a.C;
-      a.du[o] = fmaf(r, x[l * l + m], a.du[o]);
+      const int k = l * l + m;
+      a.du[st + (long long)k * a.C] = fmaf(r[l], x[k], d[k]);
     }
   }
 }
@@ -390,8 +417,14 @@ hipError_t launch_gate_backward<CGCONV_TU_L>(const GateBwdArgs& a, hipStream_t s
                      s, a.part, a.fin, a.B, a.C, chunks);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark(1);
-  hipLaunchKernelGGL(gate_bwd_kernel<CGCONV_TU_L>, gl, dim3(kGateThreads), 0, s, a, lanes);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (a.dv) {
+    hipLaunchKernelGGL((gate_bwd_kernel<CGCONV_TU_L, false>), gl, dim3(kGateThreads), 0, s, a, lanes);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (a.du) {
+    hipLaunchKernelGGL((gate_bwd_kernel<CGCONV_TU_L, true>), gl, dim3(kGateThreads), 0, s, a, lanes);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   mark(2);
   if (a.du) {
     hipLaunchKernelGGL(gate_sum_partials_kernel<CGCONV_TU_L>, g1, dim3(kGateThreads), 0, s, a.h, a.psum, a.N, a.C,
