@@ -75,6 +75,9 @@ def test_forward_and_info_reject_null_plan():
     assert "NULL" in P.cgconv_last_error()
     assert lib.cgconv_forward_bf16(None, 16, 16, 32, None) == P.CGCONV_ERR_INVALID_ARG
     assert lib.cgconv_plan_info(None, None, None, None, None) == P.CGCONV_ERR_INVALID_ARG
+    assert lib.cgconv_gate_value(None, 16, 16, 32, None) == P.CGCONV_ERR_INVALID_ARG
+    assert lib.cgconv_gate_value_backward(None, 16, 16, 32, 48, 64, None) == P.CGCONV_ERR_INVALID_ARG
+    assert "NULL" in P.cgconv_last_error()
     lib.cgconv_plan_destroy(None)  # no-op
 
 
