@@ -27,6 +27,13 @@
  * last failure on the calling thread.  No C++ exception crosses this ABI.
  * Kernel faults are asynchronous and surface at the caller's next
  * synchronisation of the stream.
+ *
+ * Graph capture: every device allocation and upload happens at plan
+ * creation; the compute entry points only enqueue kernels on the given
+ * stream (no allocation, memset, copy or host synchronisation), so a call
+ * may be captured into a HIP graph and replayed while its buffers live.
+ * Per-stage timing (cgconv_plan_enable_timing) records events and is for
+ * eager calls only.
  */
 #ifndef CGCONV_H
 #define CGCONV_H
