@@ -1,6 +1,6 @@
 """Properties of the GPU outputs that hold at any size, for the entry points
-beyond the plain forward: rotation equivariance of the backward, gating and
-graph outputs (inputs rotated by the block-diagonal Wigner matrices give
+beyond the plain forward: rotation equivariance of the backward, gating (and
+its backward) and graph outputs (inputs rotated by the block-diagonal Wigner matrices give
 outputs rotated by the same matrices, rel-L2 <= 1e-5 in fp32), run-to-run
 determinism (bitwise), and two plans driven concurrently from two streams.
 """
@@ -98,8 +98,32 @@ def test_backward_and_gate_deterministic():
     a2 = [x.cpu().numpy() for x in plan.backward(t(q), t(k), t(g))]
     f1 = plan.gate_value(t(q), t(k)).cpu().numpy()
     f2 = plan.gate_value(t(q), t(k)).cpu().numpy()
+    b1 = [x.cpu().numpy() for x in plan.gate_value_backward(t(q), t(k), t(g))]
+    b2 = [x.cpu().numpy() for x in plan.gate_value_backward(t(q), t(k), t(g))]
     plan.close()
     assert all(np.array_equal(x, y) for x, y in zip(a1, a2)) and np.array_equal(f1, f2)
+    assert all(np.array_equal(x, y) for x, y in zip(b1, b2))
+
+
+def test_gate_backward_rotation_equivariance():
+    """Both gradients of the gating step rotate with its inputs: the loss
+    <f, G> is invariant when u, v and G are rotated together, and f is
+    equivariant, so du(Du, Dv, DG) = D du and dv(Du, Dv, DG) = D dv."""
+    torch = _torch()
+    import paper_2509_24093_amd as P
+    B, N, L, C = 2, 300, 4, 3
+    u, v = W.iid(B, N, L, C, seed=7040)
+    g = np.random.default_rng(7041).normal(size=u.shape).astype(np.float32)
+    rot = _rot(L, 7042)
+    print(f"[gpu] gate backward equivariance B={B} N={N} L={L} C={C}", flush=True)
+    plan = P.Plan(B, N, L, C, boundary="linear")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    du, dv = (x.cpu().numpy() for x in plan.gate_value_backward(t(u), t(v), t(g)))
+    dur, dvr = (x.cpu().numpy() for x in plan.gate_value_backward(t(rot(u)), t(rot(v)), t(rot(g))))
+    plan.close()
+    eu, ev = rel_l2(dur, rot(du)), rel_l2(dvr, rot(dv))
+    print(f"[property] gate backward equivariance: du {eu:.3e} dv {ev:.3e}", flush=True)
+    assert eu <= 1e-5 and ev <= 1e-5
 
 
 def test_two_plans_on_two_streams():
