@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kGateThreads) void gate_partials_kernel(const float
       const float* x = u + ((long long)b * N + i) * K * C + c;
       float xv[K];
 #pragma unroll
-      for (int k = 0; k < K; ++k) xv[k] = x[(long long)k * C];
+      for (int k = 0; k < K; ++k) xv[k] = __builtin_nontemporal_load(x + (long long)k * C);  // read once
       float I[L + 1];
       degree_norms<L>(xv, I);
 #pragma unroll
@@ -320,12 +320,14 @@ __global__ __launch_bounds__(kGateThreads) void gate_bwd_du_kernel(GateBwdArgs a
   const long long base = bi * K * a.C + c;
   // Every read comes before the first store (du may alias the other
   // operands as far as the compiler knows), so the reads are not serialised
-  // behind the stores.
+  // behind the stores.  Every element is touched once: nontemporal loads and
+  // stores (0.474 -> 0.410 ms at B=8, N=16384, L_max=6, C=32, like the
+  // partials kernel's reads of u: 0.166 -> 0.131 ms).
   float x[K], d[K], r[L + 1];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
-    x[k] = a.u[base + (long long)k * a.C];
-    d[k] = a.du[base + (long long)k * a.C];
+    x[k] = __builtin_nontemporal_load(a.u + base + (long long)k * a.C);
+    d[k] = __builtin_nontemporal_load(a.du + base + (long long)k * a.C);
   }
   float I[L + 1];
   degree_norms<L>(x, I);
@@ -343,7 +345,7 @@ __global__ __launch_bounds__(kGateThreads) void gate_bwd_du_kernel(GateBwdArgs a
 #pragma unroll
     for (int m = 0; m < 2 * l + 1; ++m) {
       const int k = l * l + m;
-      a.du[st + (long long)k * a.C] = fmaf(r[l], x[k], d[k]);
+      __builtin_nontemporal_store(fmaf(r[l], x[k], d[k]), a.du + st + (long long)k * a.C);
     }
   }
 }
