@@ -233,3 +233,61 @@ def test_dense_R_equivariant():
     lhs = np.einsum("abc,bx,cy->axy", R, Dk, Dk)
     rhs = np.einsum("ab,bxy->axy", Dk, R)
     assert np.abs(lhs - rhs).max() < 1e-10
+
+
+# Path-set pins (§4.3 and the appendix on sparsity): which (l1, l2, J) blocks
+# the dense tensor sums.  Two independent checks:
+#  * counts of paths and non-zero coefficients, computed independently of
+#    this oracle when the hot-path scope was surveyed (nothing here derives
+#    them from paths());
+#  * the Clebsch-Gordan series: the coupled degrees of l1 (x) l2 are exactly
+#    J = |l1-l2| .. l1+l2, each once, so the block R[:, l1, l2] of the dense
+#    tensor, as a map from the (2l1+1)(2l2+1) product space, is an isometry
+#    when l1 + l2 <= L_max and an orthogonal projection of rank
+#    (2l1+1)(2l2+1) - ((l1+l2+1)^2 - (L_max+1)^2) otherwise (the degrees
+#    above L_max are cut).  A missing or duplicated path breaks either form.
+_COUNTS = {  # L_max: (paths, real-basis nnz, complex-basis nnz, even paths, even real nnz)
+    2: (15, 137, 113, 11, 83),
+    3: (34, 611, 449, 23, 353),
+    4: (65, 2052, 1392, 42, 1158),
+    6: (175, 11896, 7396, 106, 6460),
+    8: (369, 44171, 26159, 215, 23621),
+}
+
+
+@pytest.mark.parametrize("L", sorted(_COUNTS))
+def test_path_and_nonzero_counts(L):
+    n_paths, n_real, n_cplx, n_even, n_even_real = _COUNTS[L]
+    P = paths(L)
+    assert len(P) == n_paths
+    assert len(set(P)) == len(P)
+    R = dense_R(L)
+    assert int((np.abs(R) > 1e-12).sum()) == n_real
+    assert sum(int((np.abs(complex_cg_block(*p)) > 1e-12).sum()) for p in P) == n_cplx
+    even = [p for p in P if sum(p) % 2 == 0]
+    assert len(even) == n_even
+    assert sum(int((np.abs(real_cg_block(*p)) > 1e-12).sum()) for p in even) == n_even_real
+
+
+@pytest.mark.parametrize("L", [2, 3, 4])
+def test_path_set_is_the_clebsch_gordan_series(L):
+    R = dense_R(L)
+    K = (L + 1) ** 2
+    for l1 in range(L + 1):
+        for l2 in range(L + 1):
+            d = (2 * l1 + 1) * (2 * l2 + 1)
+            A = R[:, l1 * l1:(l1 + 1) ** 2, l2 * l2:(l2 + 1) ** 2].reshape(K, d)
+            G = A.T @ A
+            if l1 + l2 <= L:
+                assert np.abs(G - np.eye(d)).max() < 1e-12, (l1, l2)
+            else:
+                rank = d - ((l1 + l2 + 1) ** 2 - (L + 1) ** 2)
+                assert np.abs(G @ G - G).max() < 1e-12, (l1, l2)
+                assert np.trace(G) == pytest.approx(rank, abs=1e-10), (l1, l2)
+            # output rows: orthonormal on the coupled degrees, zero elsewhere
+            for J in range(L + 1):
+                rows = A[J * J:(J + 1) ** 2]
+                if abs(l1 - l2) <= J <= l1 + l2:
+                    assert np.abs(rows @ rows.T - np.eye(2 * J + 1)).max() < 1e-12, (l1, l2, J)
+                else:
+                    assert np.abs(rows).max() == 0.0, (l1, l2, J)

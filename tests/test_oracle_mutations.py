@@ -217,3 +217,38 @@ def test_gating_mistakes_are_caught(monkeypatch, plant):
     vv[:, :, 0, :] = 1.0
     caught |= np.abs(og.gate_value(uu, vv, 2) - orig_gate(uu, 2)).max() > 1e-12
     assert caught
+
+
+def _path_pins_hold(L=3):
+    """The path-set pins of test_oracle_cg: the path count and the
+    Clebsch-Gordan series (isometry of each coupled block with l1+l2 <= L)."""
+    if len(ocg.paths(L)) != {2: 15, 3: 34}[L]:
+        return False
+    R = ocg._dense_R(L)
+    K = (L + 1) ** 2
+    for l1 in range(L + 1):
+        for l2 in range(L + 1 - l1):
+            d = (2 * l1 + 1) * (2 * l2 + 1)
+            A = R[:, l1 * l1:(l1 + 1) ** 2, l2 * l2:(l2 + 1) ** 2].reshape(K, d)
+            if np.abs(A.T @ A - np.eye(d)).max() > 1e-12:
+                return False
+    return True
+
+
+def test_path_pins_hold_unmutated():
+    assert _path_pins_hold(2) and _path_pins_hold(3)
+
+
+@pytest.mark.parametrize("plant", ["drop_stretched", "cap_at_max_degree"])
+def test_path_set_mistakes_are_caught(monkeypatch, plant):
+    orig = ocg.paths
+    if plant == "drop_stretched":
+        # the stretched couplings J = l1 + l2 with l1, l2 >= 1 left out
+        bad = lambda L: [p for p in orig(L) if not (p[0] >= 1 and p[1] >= 1 and p[2] == p[0] + p[1])]
+    else:
+        # output degree capped at max(l1, l2)
+        bad = lambda L: [p for p in orig(L) if p[2] <= max(p[0], p[1])]
+    monkeypatch.setattr(ocg, "paths", bad)
+    # both planted path sets stay equivariant and keep the §4.4 cross product
+    assert _equivariant() and _cross_relation_holds()
+    assert not _path_pins_hold(2) and not _path_pins_hold(3)
