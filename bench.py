@@ -331,8 +331,10 @@ def main():
     if args.gate_backward:
         bench_gate_backward(args, plan, q, k, qd, kd, B, N, L, C)
         return
-    n_paths, nnz, n_products, ws_bytes = plan.info()
-    log(f"[bench] plan: paths={n_paths} nnz={nnz} products={n_products} workspace={ws_bytes / 2**30:.2f} GiB")
+    n_paths, nnz_real, ws_bytes = plan.info()
+    nnz, n_products = plan.contraction_info()
+    log(f"[bench] plan: paths={n_paths} nnz={nnz_real} real / {nnz} complex-basis, products={n_products} "
+        f"workspace={ws_bytes / 2**30:.2f} GiB")
 
     for _ in range(args.warmup):
         plan(qd, kd, out)
@@ -560,7 +562,7 @@ def bench_backward(args, plan, q, k, qd, kd, B, N, L, C):
                           stream)
     log(f"[bench] timing {args.steps} backward steps")
     ms, stage_avg = _timed(args, step, plan, calls_per_step=2)
-    _, nnz, n_products, _ = plan.info()
+    nnz, n_products = plan.contraction_info()
     counters, src = committed_counters(args.workload)
     if args.boundary != "cyclic":
         counters, src = None, "counters were taken with the cyclic boundary"

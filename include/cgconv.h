@@ -216,7 +216,7 @@ int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const fl
                     float* grad_q, float* grad_k, hipStream_t stream);
 
 /*
- * Invariant softmax gating and the real-space value tensor product (§4.2
+ * Invariant softmax gating and the real-space value tensor product (§4.1.1
  * Invariant Gating; Algorithm 1, step 5), for the plan's batch, N, L_max, C:
  *
  *   I[b,i,l,c]     = || u[b,i,(l,.),c] ||_2          (norm over the 2l+1 components)
@@ -264,14 +264,39 @@ int64_t cgconv_paths(int32_t L_max, int32_t* l1l2J, int64_t cap);
 void cgconv_plan_destroy(cgconv_plan_t plan);
 
 /*
- * Plan introspection: number of CG paths (l1,l2,J); number of non-zero
- * complex-basis coefficients the kernels evaluate per frequency and channel
- * (selection rule M = m1 + m2, §4.3); number of distinct complex products
- * q[l1,m1] * k[l2,m2] among them; workspace bytes.  Any output pointer may be
- * NULL.
+ * Plan introspection: number of CG paths (l1,l2,J) (§4.1, the path sum);
+ * number of non-zero real-basis coefficients of the tensor the plan's
+ * kernels evaluate (the entries cgconv_plan_export_table writes; §4.3 and
+ * the appendix on sparsity, real basis); workspace bytes.  Any output
+ * pointer may be NULL.  Returns 0, or CGCONV_ERR_INVALID_ARG for a NULL plan.
  */
-int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths, int64_t* nnz, int64_t* n_products,
-                     size_t* workspace_bytes);
+int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths, int64_t* nnz, size_t* workspace_bytes);
+
+/*
+ * The form in which the kernels of a token plan evaluate that tensor: the
+ * number of complex-basis terms (selection rule M = m1 + m2, §4.3) and of
+ * distinct complex products q[l1,m1] * k[l2,m2] among them, per frequency
+ * and channel.  (A graph plan reports the same counts; its per-frequency
+ * product runs on the real-basis entries.)  Either pointer may be NULL.
+ */
+int cgconv_plan_contraction_info(cgconv_plan_t plan, int64_t* nnz_complex, int64_t* n_products);
+
+/*
+ * Export the real-basis CG tensor R^{(l1 l2 J)}[M,m1,m2] that the plan's
+ * kernels evaluate (§4.1 Eq. (EquiConv) summed over the paths; the sparse
+ * entries of §4.3).  For a token plan it is recovered from the plan's
+ * complex-basis contraction terms (the table the generated and the
+ * table-driven kernels are built from) by expanding them back to the real
+ * basis; for a graph plan it is the real table of its per-frequency
+ * product.  Writes up to `cap` entries: l1m1l2m2JM[6*e .. 6*e+5] =
+ * (l1, m1, l2, m2, J, M) and coef[e] (double), every |coef| > 1e-12, sorted
+ * by (J, M, l1, m1, l2, m2); both buffers are HOST memory owned by the
+ * caller and may be NULL when cap == 0.  Returns the total number of entries
+ * (= cgconv_plan_info's nnz; it may exceed cap, nothing beyond cap is
+ * written), or CGCONV_ERR_INVALID_ARG (NULL plan, cap < 0, NULL buffer with
+ * cap > 0).  Host-only: no device work.
+ */
+int64_t cgconv_plan_export_table(cgconv_plan_t plan, int32_t* l1m1l2m2JM, double* coef, int64_t cap);
 
 /*
  * Host-only (no GPU needed): the real-basis CG tensor R for degrees 0..L_max

@@ -1,7 +1,7 @@
 """Invariant softmax gating and the real-space value tensor product, for the
 oracle (test infrastructure only).
 
-Paper §4.2 (Invariant Gating) and Algorithm 1, step 5: after the CG
+Paper §4.1.1 (Invariant Gating) and Algorithm 1, step 5: after the CG
 convolution u, invariant features I^l = gamma^l(u^0, u^1, ...) are formed,
 one per degree l, of dimension N x m_l; the gated features sigma(I^l) u^l
 are combined with the values v by a second CG tensor product taken in real

@@ -75,9 +75,12 @@ def library() -> ctypes.CDLL:
     lib.cgconv_paths.restype = i64
     lib.cgconv_plan_destroy.argtypes = [vp]
     lib.cgconv_plan_destroy.restype = None
-    lib.cgconv_plan_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64),
-                                     ctypes.POINTER(sz)]
+    lib.cgconv_plan_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(sz)]
     lib.cgconv_plan_info.restype = ctypes.c_int
+    lib.cgconv_plan_contraction_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.cgconv_plan_contraction_info.restype = ctypes.c_int
+    lib.cgconv_plan_export_table.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double), i64]
+    lib.cgconv_plan_export_table.restype = i64
     lib.cgconv_cg_table.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double), i64]
     lib.cgconv_cg_table.restype = i64
     lib.cgconv_contract_host.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
@@ -187,10 +190,33 @@ def cgconv_plan_destroy(plan: int) -> None:
 
 
 def cgconv_plan_info(plan: int):
-    """Returns (n_paths, nnz, n_products, workspace_bytes)."""
-    a, b, c, d = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_size_t()
-    _check(library().cgconv_plan_info(plan, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c), ctypes.byref(d)))
-    return a.value, b.value, c.value, d.value
+    """Returns (n_paths, nnz, workspace_bytes); nnz counts the real-basis
+    entries of the tensor the plan evaluates."""
+    a, b, d = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_size_t()
+    _check(library().cgconv_plan_info(plan, ctypes.byref(a), ctypes.byref(b), ctypes.byref(d)))
+    return a.value, b.value, d.value
+
+
+def cgconv_plan_contraction_info(plan: int):
+    """Returns (complex-basis terms, distinct complex products) of the plan's
+    contraction."""
+    a, b = ctypes.c_int64(), ctypes.c_int64()
+    _check(library().cgconv_plan_contraction_info(plan, ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
+
+
+def cgconv_plan_export_table(plan: int):
+    """The real-basis tensor the plan evaluates (host copy).
+    Returns (idx int32 (n, 6) = l1, m1, l2, m2, J, M; coef float64 (n,))."""
+    import numpy as np
+    lib = library()
+    n = _check(lib.cgconv_plan_export_table(plan, None, None, 0))
+    idx = np.zeros((n, 6), dtype=np.int32)
+    coef = np.zeros(n, dtype=np.float64)
+    got = _check(lib.cgconv_plan_export_table(plan, idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                              coef.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), n))
+    assert got == n
+    return idx, coef
 
 
 def cgconv_plan_enable_timing(plan: int, max_calls: int) -> None:
@@ -252,7 +278,15 @@ class Plan:
         self._h = cgconv_plan_create_boundary(int(batch), int(N), int(L_max), int(C), code)
 
     def info(self):
+        """(n_paths, nnz real-basis, workspace_bytes)."""
         return cgconv_plan_info(self._h)
+
+    def contraction_info(self):
+        """(complex-basis terms, distinct complex products)."""
+        return cgconv_plan_contraction_info(self._h)
+
+    def export_table(self):
+        return cgconv_plan_export_table(self._h)
 
     def enable_timing(self, max_calls: int):
         cgconv_plan_enable_timing(self._h, max_calls)

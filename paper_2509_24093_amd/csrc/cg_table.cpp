@@ -133,6 +133,85 @@ std::vector<Term> contraction_terms(int L) {
   return out;
 }
 
+bool evaluated_table(int L, const std::vector<Term>& terms, std::vector<RealEntry>& out) {
+  out.clear();
+  const int K = (L + 1) * (L + 1);
+  const std::complex<double> I(0.0, 1.0);
+  // qa[comp(l, m)] = sum_x A[m][x] q[x] over the (at most two) real components
+  // x of degree l with |m_x| = |m|; the same map gives ka from k
+  struct Lin {
+    int n;
+    int x[2];
+    std::complex<double> a[2];
+  };
+  auto in_map = [&](int l, int m) {
+    Lin r;
+    if (m == 0) {
+      r.n = 1;
+      r.x[0] = comp(l, 0);
+      r.a[0] = 2.0;
+    } else {
+      const int mu = m < 0 ? -m : m;
+      r.n = 2;
+      r.x[0] = comp(l, mu);
+      r.a[0] = 2.0;
+      r.x[1] = comp(l, -mu);
+      r.a[1] = m < 0 ? 2.0 * I : -2.0 * I;
+    }
+    return r;
+  };
+  // U[y] = sum_o B[y][o] w[o]: output w[J, M] reaches the real components
+  // (J, 0) for M = 0, and (J, +mu) with weight 1 and (J, -mu) with weight
+  // +i (M = +mu) or -i (M = -mu)
+  auto out_map = [&](int J, int M) {
+    Lin r;
+    if (M == 0) {
+      r.n = 1;
+      r.x[0] = comp(J, 0);
+      r.a[0] = 1.0;
+    } else {
+      const int mu = M < 0 ? -M : M;
+      r.n = 2;
+      r.x[0] = comp(J, mu);
+      r.a[0] = 1.0;
+      r.x[1] = comp(J, -mu);
+      r.a[1] = M > 0 ? I : -I;
+    }
+    return r;
+  };
+  std::vector<std::complex<double>> R((size_t)K * K * K, 0.0);
+  for (const Term& t : terms) {
+    const std::complex<double> c = t.imag ? I * t.coef : std::complex<double>(t.coef, 0.0);
+    const Lin o = out_map(t.J, t.M), a = in_map(t.l1, t.m1), b = in_map(t.l2, t.m2);
+    for (int i = 0; i < o.n; ++i)
+      for (int j = 0; j < a.n; ++j)
+        for (int k = 0; k < b.n; ++k)
+          R[((size_t)o.x[i] * K + a.x[j]) * K + b.x[k]] += o.a[i] * c * a.a[j] * b.a[k];
+  }
+  auto degree = [](int x, int& l, int& m) {
+    l = 0;
+    while ((l + 1) * (l + 1) <= x) ++l;
+    m = x - l * l - l;
+  };
+  for (int y = 0; y < K; ++y)
+    for (int x1 = 0; x1 < K; ++x1)
+      for (int x2 = 0; x2 < K; ++x2) {
+        const std::complex<double> v = R[((size_t)y * K + x1) * K + x2];
+        if (std::abs(v.imag()) > 1e-12) {
+          out.clear();
+          return false;
+        }
+        if (std::abs(v.real()) <= 1e-12) continue;
+        RealEntry e;
+        degree(y, e.J, e.M);
+        degree(x1, e.l1, e.m1);
+        degree(x2, e.l2, e.m2);
+        e.coef = v.real();
+        out.push_back(e);
+      }
+  return true;
+}
+
 void contract_host(int L, const std::complex<double>* qhat, const std::complex<double>* khat,
                    std::complex<double>* uhat) {
   const int K = (L + 1) * (L + 1);

@@ -44,6 +44,15 @@ struct Term {
 };
 std::vector<Term> contraction_terms(int L);
 
+// The real-basis tensor that a list of contraction terms evaluates: the
+// terms expanded back through the change to the idempotent complex-m
+// components and the return to the real basis (the maps written out above
+// contraction_terms), entries with |coef| > 1e-12, sorted by
+// (J, M, l1, m1, l2, m2).  Returns false (and an empty table) if an expanded
+// coefficient is not real, which would mean the terms are not those of a
+// real-basis tensor.
+bool evaluated_table(int L, const std::vector<Term>& terms, std::vector<RealEntry>& out);
+
 // Number of triangle paths (l1, l2, J) with all degrees <= L.
 int64_t n_paths(int L);
 

@@ -73,7 +73,9 @@ struct cgconv_plan {
   int64_t N1 = 0, N2 = 0;  // N1 == 0: single pass
   bool fused = false;      // two-pass with N2 = 64 and the fused middle kernel
   int device = 0;
-  int64_t nnz = 0, paths = 0, products = 0;
+  int64_t nnz = 0, paths = 0, products = 0;  // nnz: complex-basis terms the contraction evaluates
+  // the real-basis tensor the plan's kernels evaluate (cgconv_plan_export_table)
+  std::vector<RealEntry> rtable;
   size_t ws_bytes = 0;
   float2* tw = nullptr;
   float2* ws1 = nullptr;
@@ -562,6 +564,11 @@ cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32
     }
   }
   p->nnz = (int64_t)terms.size();
+  if (!evaluated_table(L_max, terms, p->rtable)) {
+    set_error("internal error: the contraction terms do not expand to a real tensor");
+    delete p;
+    return nullptr;
+  }
   {
     std::vector<char> seen((size_t)K * K, 0);
     for (const Term& t : terms) {
@@ -651,6 +658,7 @@ cgconv_plan_t cgconv_plan_create_graph(int64_t batch, int64_t N, int32_t L_max, 
   p->K = K;
   p->paths = n_paths(L_max);
   p->nnz = (int64_t)contraction_terms(L_max).size();
+  p->rtable = real_table(L_max);  // the per-frequency product is the generated real-basis body
   p->Kp = round_up(N, 32);
   p->Mp = round_up(N, 128);
   p->KCp = round_up((int64_t)K * C, 128);
@@ -877,17 +885,44 @@ int cgconv_backward_graph(cgconv_plan_t plan, const float* U, const float* q, co
   return CGCONV_OK;
 }
 
-int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths_out, int64_t* nnz, int64_t* n_products,
-                     size_t* workspace_bytes) {
+int cgconv_plan_info(cgconv_plan_t plan, int64_t* n_paths_out, int64_t* nnz, size_t* workspace_bytes) {
   if (!plan) {
     set_error("plan is NULL");
     return CGCONV_ERR_INVALID_ARG;
   }
   if (n_paths_out) *n_paths_out = plan->paths;
-  if (nnz) *nnz = plan->nnz;
-  if (n_products) *n_products = plan->products;
+  if (nnz) *nnz = (int64_t)plan->rtable.size();
   if (workspace_bytes) *workspace_bytes = plan->ws_bytes;
   return CGCONV_OK;
+}
+
+int cgconv_plan_contraction_info(cgconv_plan_t plan, int64_t* nnz_complex, int64_t* n_products) {
+  if (!plan) {
+    set_error("plan is NULL");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (nnz_complex) *nnz_complex = plan->nnz;
+  if (n_products) *n_products = plan->products;
+  return CGCONV_OK;
+}
+
+int64_t cgconv_plan_export_table(cgconv_plan_t plan, int32_t* l1m1l2m2JM, double* coef, int64_t cap) {
+  if (!plan) {
+    set_error("plan is NULL");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (cap < 0 || (cap > 0 && (!l1m1l2m2JM || !coef))) {
+    set_error("invalid output buffers");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const std::vector<RealEntry>& t = plan->rtable;
+  for (int64_t e = 0; e < (int64_t)t.size() && e < cap; ++e) {
+    const RealEntry& r = t[e];
+    const int32_t v[6] = {r.l1, r.m1, r.l2, r.m2, r.J, r.M};
+    std::memcpy(l1m1l2m2JM + 6 * e, v, sizeof v);
+    coef[e] = r.coef;
+  }
+  return (int64_t)t.size();
 }
 
 int cgconv_plan_enable_timing(cgconv_plan_t plan, int32_t max_calls) {

@@ -74,7 +74,9 @@ def test_forward_and_info_reject_null_plan():
     assert lib.cgconv_forward(None, 16, 16, 32, None) == P.CGCONV_ERR_INVALID_ARG
     assert "NULL" in P.cgconv_last_error()
     assert lib.cgconv_forward_bf16(None, 16, 16, 32, None) == P.CGCONV_ERR_INVALID_ARG
-    assert lib.cgconv_plan_info(None, None, None, None, None) == P.CGCONV_ERR_INVALID_ARG
+    assert lib.cgconv_plan_info(None, None, None, None) == P.CGCONV_ERR_INVALID_ARG
+    assert lib.cgconv_plan_contraction_info(None, None, None) == P.CGCONV_ERR_INVALID_ARG
+    assert lib.cgconv_plan_export_table(None, None, None, 0) == P.CGCONV_ERR_INVALID_ARG
     assert lib.cgconv_gate_value(None, 16, 16, 32, None) == P.CGCONV_ERR_INVALID_ARG
     assert lib.cgconv_gate_value_backward(None, 16, 16, 32, 48, 64, None) == P.CGCONV_ERR_INVALID_ARG
     assert "NULL" in P.cgconv_last_error()
@@ -143,3 +145,45 @@ def test_graph_entry_points_reject_bad_arguments():
     lib = P.library()
     assert lib.cgconv_forward_graph(None, 16, 32, 48, 64, None) == P.CGCONV_ERR_INVALID_ARG
     assert lib.cgconv_backward_graph(None, 16, 32, 48, 64, 80, 96, None) == P.CGCONV_ERR_INVALID_ARG
+
+
+def _dense_from_entries(idx, coef, L):
+    K = (L + 1) ** 2
+    R = np.zeros((K, K, K))
+    for (l1, m1, l2, m2, J, M), c in zip(idx, coef):
+        R[J * J + J + M, l1 * l1 + l1 + m1, l2 * l2 + l2 + m2] += c
+    return R
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 4, 5, 6, 7, 8])
+def test_plan_export_table_matches_oracle(L):
+    """The tensor a plan's kernels evaluate, exported through the C ABI,
+    equals the oracle's dense R (entries, count, order), for a token plan
+    (recovered from its contraction terms) and a graph plan."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("plan creation needs a GPU")
+    torch.cuda.set_device(0)
+    print(f"[gpu] export table L={L}", flush=True)
+    R = dense_R(L)
+    n_ref = int((np.abs(R) > 1e-12).sum())
+    for plan in (P.Plan(1, 64, L, 2), P.GraphPlan(1, 16, L, 2)):
+        try:
+            n_paths, nnz, ws = plan.info()
+            idx, coef = plan.export_table()
+            assert nnz == len(coef) == n_ref
+            assert np.abs(_dense_from_entries(idx, coef, L) - R).max() < 1e-12
+            keys = [tuple(r) for r in idx[:, [4, 5, 0, 1, 2, 3]]]
+            assert keys == sorted(keys)
+            assert n_paths == len(P.cgconv_paths(L))
+            nc, npr = plan.contraction_info()
+            assert nc > 0 and 0 < npr <= nc
+            # a short buffer: the full count comes back, nothing past cap is written
+            lib = P.library()
+            ib = (ctypes.c_int32 * 12)(*([-7] * 12))
+            cb = (ctypes.c_double * 3)(9.0, 9.0, 9.0)
+            assert lib.cgconv_plan_export_table(plan._h, ib, cb, 1 if n_ref > 1 else 0) == n_ref
+            assert cb[1] == 9.0 and ib[6] == -7
+        finally:
+            plan.close()

@@ -234,8 +234,9 @@ def test_argument_errors_on_gpu():
     import paper_2509_24093_amd as P
     print("[gpu] argument errors (no kernel launched)", flush=True)
     plan = P.Plan(1, 64, 2, 4)
-    n_paths, nnz, n_products, ws = plan.info()
-    assert n_paths == 15 and nnz == 113 and n_products == 71 and ws > 0
+    n_paths, nnz, ws = plan.info()
+    assert n_paths == 15 and nnz == 137 and ws > 0
+    assert plan.contraction_info() == (113, 71)
     buf = torch.zeros(1 * 64 * 9 * 4 + 8, device="cuda")
     base = buf.data_ptr()
     lib = P.library()
