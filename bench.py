@@ -61,7 +61,10 @@ METRIC_GATE = "invariant softmax gating + value tensor product, tokens/sec at N=
 METRIC_GATE_BACKWARD = ("gating + value tensor product backward (grad_u and grad_v), tokens/sec at N=16384, "
                         "L_max=6, C=32")
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
+# sources of every kernel of the fused forward (the step's counter bytes
+# cover all three stages) and of the plan that launches them
 CG_SOURCES = ["paper_2509_24093_amd/csrc/cg_gen.hip", "paper_2509_24093_amd/csrc/cg_fused.hip",
+              "paper_2509_24093_amd/csrc/fft.hip", "paper_2509_24093_amd/csrc/cgconv.cpp",
               "paper_2509_24093_amd/csrc/cg_common.h", "paper_2509_24093_amd/csrc/fft_reg.h",
               "paper_2509_24093_amd/csrc/codegen/gen_cg.cpp", "paper_2509_24093_amd/csrc/cg_table.cpp",
               "paper_2509_24093_amd/csrc/kernels.h"]
@@ -129,6 +132,48 @@ def copy_peak_gbs(nbytes=1 << 30, reps=10):
     ms = e0.elapsed_time(e1) / reps
     del src, dst
     return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def hbm_ceiling(nbytes=1 << 30, reps=10):
+    """Measured HBM ceiling: the hand-written streaming kernels of
+    libhbmprobe.so (16-byte accesses: copy, copy with nontemporal loads and
+    stores, read only, write only), each at a few grid sizes, timed with HIP
+    events on the current stream after warm-up launches, next to torch's
+    device copy.  Returns {name: GB/s (bytes read + written per second)} with
+    the grid size of each best result."""
+    import ctypes
+
+    import torch
+    from paper_2509_24093_amd.build import PROBE_LIB
+    lib = ctypes.CDLL(PROBE_LIB)
+    lib.hbm_probe.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
+                              ctypes.c_void_p]
+    lib.hbm_probe.restype = ctypes.c_int
+    src = torch.ones(nbytes // 4, device="cuda")
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream().cuda_stream
+    out = {}
+    for mode, name, moved in ((0, "copy", 2), (1, "copy_nontemporal", 2), (2, "read", 1), (3, "write", 1)):
+        best = (0.0, 0)
+        for blocks in (1024, 2048, 4096, 8192):
+            def launch():
+                if lib.hbm_probe(src.data_ptr(), dst.data_ptr(), nbytes, mode, blocks, stream) != 0:
+                    raise RuntimeError("hbm_probe launch failed")
+            for _ in range(2):
+                launch()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                launch()
+            e1.record()
+            torch.cuda.synchronize()
+            gbs = moved * nbytes / (e0.elapsed_time(e1) / reps * 1e-3) / 1e9
+            best = max(best, (gbs, blocks))
+        out[name + "_gbs"] = round(best[0], 1)
+        out[name + "_blocks"] = best[1]
+    del src, dst
+    out["torch_copy_gbs"] = round(copy_peak_gbs(nbytes, reps), 1)
+    return out
 
 
 def cpu_baseline(q, k, L, budget_s, got, linear=False):
@@ -336,20 +381,8 @@ def main():
     log(f"[bench] plan: paths={n_paths} nnz={nnz_real} real / {nnz} complex-basis, products={n_products} "
         f"workspace={ws_bytes / 2**30:.2f} GiB")
 
-    for _ in range(args.warmup):
-        plan(qd, kd, out)
-    torch.cuda.synchronize()
-    plan.enable_timing(args.steps)
     log(f"[bench] timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        plan(qd, kd, out)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-    stage_ms, ncalls = plan.stage_times()
-    stage_avg = {s: v / max(ncalls, 1) for s, v in stage_ms.items()}
+    ms, stage_avg, timing = _timed(args, lambda: plan(qd, kd, out), plan)
     tokens = B * N
     S = B * N * K * C * esize                     # one feature tensor in bytes
     # bytes each kernel must move (inputs read + outputs written), fp32
@@ -373,8 +406,11 @@ def main():
     roofline = cg_roofline(stage_avg, B, Nf, L, C, n_products, nnz,
                            counters["cg_hbm_bytes_per_launch"] if counters else None, traffic_src)
     hbm_alg_gbs = 3 * S / (ms * 1e-3) / 1e9
-    copy_gbs = copy_peak_gbs()
-    log(f"[bench] device copy of 1 GiB: {copy_gbs:.0f} GB/s")
+    ceiling = hbm_ceiling()
+    copy_gbs = max(ceiling["copy_gbs"], ceiling["copy_nontemporal_gbs"], ceiling["torch_copy_gbs"])
+    log(f"[bench] HBM ceiling (1 GiB): copy {ceiling['copy_gbs']:.0f}, nontemporal copy "
+        f"{ceiling['copy_nontemporal_gbs']:.0f}, read {ceiling['read_gbs']:.0f}, write {ceiling['write_gbs']:.0f}, "
+        f"torch copy {ceiling['torch_copy_gbs']:.0f} GB/s")
     for st in stages.values():
         st["frac_of_copy"] = round(st["gbs"] / copy_gbs, 4) if st.get("bytes") else None
     result = {
@@ -398,11 +434,13 @@ def main():
                 "counter_gbs": round(counters["step_hbm_bytes"] / (ms * 1e-3) / 1e9, 1) if counters else None,
                 "counter_frac": round(counters["step_hbm_bytes"] / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4)
                 if counters else None,
-                "copy_measured_gbs": round(copy_gbs, 1), "frac_of_copy": round(hbm_alg_gbs / copy_gbs, 4),
+                "copy_measured_gbs": round(copy_gbs, 1), "ceiling": ceiling,
+                "frac_of_copy": round(hbm_alg_gbs / copy_gbs, 4),
                 "counter_frac_of_copy": round(counters["step_hbm_bytes"] / (ms * 1e-3) / 1e9 / copy_gbs, 4)
                 if counters else None},
         "roofline": roofline,
         "stages": stages,
+        "timing": timing,
     }
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle baseline (~{args.cpu_seconds:.0f} s)")
@@ -436,18 +474,8 @@ def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
     n_paths = len(paths)
     wts = (np.random.default_rng(2025).normal(size=(n_paths, C, C)) / np.sqrt(C)).astype(np.float32)
     wd = torch.from_numpy(wts).cuda()
-    for _ in range(args.warmup):
-        plan.forward_mixed(qd, kd, wd, out)
-    torch.cuda.synchronize()
-    plan.enable_timing(args.steps)
     log(f"[bench] timing {args.steps} mixed steps")
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        plan.forward_mixed(qd, kd, wd, out)
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / args.steps
-    stage_ms, ncalls = plan.stage_times()
-    stage_avg = {s: v / max(ncalls, 1) for s, v in stage_ms.items()}
+    ms, stage_avg, timing = _timed(args, lambda: plan.forward_mixed(qd, kd, wd, out), plan)
     mix_ms = stage_avg["cg_mix"]
     F = N // 2 + 1
     pts = B * F
@@ -457,6 +485,7 @@ def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
     mfma_flops = 6 * 32 * 32 * 16 * 2 * pair_tiles * ((pts + 7) // 8)  # bf16 MFMAs executed
     achieved = mfma_flops / (mix_ms * 1e-3) / 1e12
     result = {
+        "timing": timing,
         "metric": METRIC_MIXED,
         "value": B * N / (ms * 1e-3),
         "unit": "tokens/s",
@@ -519,29 +548,50 @@ def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
     print(json.dumps(result), flush=True)
 
 
-def _common(args, metric, ms, B, N, L, C, dtype):
-    return {"metric": metric, "value": B * N / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+def _common(args, metric, ms, B, N, L, C, dtype, timing=None):
+    r = {"metric": metric, "value": B * N / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": dtype, "data": "synthetic",
             "config": {"workload": args.workload, "batch": B, "N": N, "L_max": L, "C": C, "boundary": args.boundary,
                        "parallelism": "single GPU"}}
+    if timing is not None:
+        r["timing"] = timing
+    return r
 
 
 def _timed(args, step, plan, calls_per_step=1):
-    """Warm up, then time args.steps calls of step() with the plan's stage
-    timing on; returns (ms per step, {stage: average ms per timed call})."""
+    """Warm up, then time args.steps calls of step(), each between two HIP
+    events on the current stream (the one the library enqueues on), with the
+    plan's stage timing off; the host synchronises before and after the
+    timed steps.  Then a separate pass of up to 20 steps with the stage
+    timing on gives the per-kernel averages.  Returns (median ms per step,
+    {stage: average ms per timed call}, timing record)."""
     import torch
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    plan.enable_timing(args.steps * calls_per_step)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for a, b in ev:
+        a.record()
         step()
+        b.record()
     torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    per_step = sorted(a.elapsed_time(b) for a, b in ev)
+    ms = per_step[len(per_step) // 2] if len(per_step) % 2 else 0.5 * (per_step[len(per_step) // 2 - 1] +
+                                                                          per_step[len(per_step) // 2])
+    n_stage = min(args.steps, 20)
+    plan.enable_timing(n_stage * calls_per_step)
+    for _ in range(n_stage):
+        step()
     stage_ms, ncalls = plan.stage_times()
-    return ms, {s: v / max(ncalls, 1) for s, v in stage_ms.items()}
+    plan.enable_timing(0)
+    rec = {"method": f"HIP events around each of the {args.steps} timed steps on the stream the kernels run on; "
+                     f"median; stage times from a separate pass of {n_stage} steps",
+           "median_ms": round(ms, 4), "min_ms": round(per_step[0], 4), "max_ms": round(per_step[-1], 4),
+           "wall_ms_per_step": round(wall_ms, 4)}
+    return ms, {s: v / max(ncalls, 1) for s, v in stage_ms.items()}, rec
 
 
 def bench_backward(args, plan, q, k, qd, kd, B, N, L, C):
@@ -561,7 +611,7 @@ def bench_backward(args, plan, q, k, qd, kd, B, N, L, C):
         P.cgconv_backward(plan._h, qd.data_ptr(), kd.data_ptr(), gd.data_ptr(), gq.data_ptr(), gk.data_ptr(),
                           stream)
     log(f"[bench] timing {args.steps} backward steps")
-    ms, stage_avg = _timed(args, step, plan, calls_per_step=2)
+    ms, stage_avg, timing = _timed(args, step, plan, calls_per_step=2)
     nnz, n_products = plan.contraction_info()
     counters, src = committed_counters(args.workload)
     if args.boundary != "cyclic":
@@ -569,7 +619,7 @@ def bench_backward(args, plan, q, k, qd, kd, B, N, L, C):
     roofline = cg_roofline(stage_avg, B, dft_length(N, args.boundary), L, C, n_products, nnz,
                            counters["cg_hbm_bytes_per_launch"] if counters else None,
                            (src + "; taken on the forward, same kernel and launch shape") if counters else src)
-    result = _common(args, METRIC_BACKWARD, ms, B, N, L, C, "f32")
+    result = _common(args, METRIC_BACKWARD, ms, B, N, L, C, "f32", timing)
     result["roofline"] = roofline
     result["stages_per_gradient"] = {s: {"ms": round(t, 4)} for s, t in stage_avg.items()}
     if not args.no_cpu_baseline:
@@ -607,7 +657,7 @@ def bench_gate(args, plan, q, k, qd, kd, out, B, N, L, C):
 
     import paper_2509_24093_amd as P
     log(f"[bench] timing {args.steps} gating steps")
-    ms, stage_avg = _timed(args, lambda: plan.gate_value(qd, kd, out), plan)
+    ms, stage_avg, timing = _timed(args, lambda: plan.gate_value(qd, kd, out), plan)
     K = (L + 1) ** 2
     _, coef = P.cgconv_cg_table(L)
     nnz_real = len(coef)
@@ -616,7 +666,7 @@ def bench_gate(args, plan, q, k, qd, kd, out, B, N, L, C):
     flops = per_lane * lanes
     gv_ms = stage_avg["gate_value"]
     achieved = flops / (gv_ms * 1e-3) / 1e12
-    result = _common(args, METRIC_GATE, ms, B, N, L, C, "f32")
+    result = _common(args, METRIC_GATE, ms, B, N, L, C, "f32", timing)
     result["roofline"] = {
         "kernel": f"gate_value_kernel<{L}>",
         "bound": "alu",
@@ -678,7 +728,7 @@ def bench_gate_backward(args, plan, q, k, qd, kd, B, N, L, C):
         P.cgconv_gate_value_backward(plan._h, qd.data_ptr(), kd.data_ptr(), gd.data_ptr(), gu.data_ptr(),
                                      gv.data_ptr(), stream)
     log(f"[bench] timing {args.steps} gating backward steps")
-    ms, stage_avg = _timed(args, step, plan)
+    ms, stage_avg, timing = _timed(args, step, plan)
     K = (L + 1) ** 2
     _, coef = P.cgconv_cg_table(L)
     nnz_real = len(coef)
@@ -687,7 +737,7 @@ def bench_gate_backward(args, plan, q, k, qd, kd, B, N, L, C):
     flops = per_lane * lanes
     bw_ms = stage_avg["gate_bwd"]
     achieved = flops / (bw_ms * 1e-3) / 1e12
-    result = _common(args, METRIC_GATE_BACKWARD, ms, B, N, L, C, "f32")
+    result = _common(args, METRIC_GATE_BACKWARD, ms, B, N, L, C, "f32", timing)
     result["roofline"] = {
         "kernel": f"gate_bwd_kernel<{L}, false> + gate_bwd_kernel<{L}, true> (one launch per gradient)",
         "bound": "alu",
@@ -753,7 +803,7 @@ def bench_graph(args):
     plan = P.GraphPlan(B, N, L, C)
     out = torch.empty_like(qd)
     log(f"[bench] timing {args.steps} graph steps")
-    ms, stage_avg = _timed(args, lambda: plan(Ud, qd, kd, out), plan)
+    ms, stage_avg, timing = _timed(args, lambda: plan(Ud, qd, kd, out), plan)
     K = (L + 1) ** 2
     Kp = -(-N // 32) * 32
     Mp = -(-N // 128) * 128
@@ -762,7 +812,7 @@ def bench_graph(args):
     fp32_equiv = 2 * N * N * (2 * K * C) * B             # the transform itself
     gm = stage_avg["gft_gemm_fwd"]
     achieved = mfma_flops / (gm * 1e-3) / 1e12
-    result = _common(args, METRIC_GRAPH, ms, B, N, L, C, "f32 (transforms: bf16 hi/lo split on MFMA, fp32 accumulate)")
+    result = _common(args, METRIC_GRAPH, ms, B, N, L, C, "f32 (transforms: bf16 hi/lo split on MFMA, fp32 accumulate)", timing)
     result["config"] = {"workload": "graph", "batch": B, "N": N, "L_max": L, "C": C,
                         "basis": "normalised Laplacian eigenvectors of the 16-NN graph", "parallelism": "single GPU"}
     result["roofline"] = {

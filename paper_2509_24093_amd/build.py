@@ -18,6 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcgconv.so")
+PROBE_LIB = os.path.join(HERE, "libhbmprobe.so")  # the benchmark's HBM-ceiling kernels
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LGEN = 8  # highest L_max with a generated register-resident contraction
 FUSED_LMAX = 6  # highest L_max with a fused (second pass + CG + inverse first pass) kernel
@@ -84,6 +85,9 @@ def build(jobs: int | None = None, verbose: bool = True) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs, verbose)
     os.replace(tmp, LIB)
+    tmp = PROBE_LIB + ".tmp"
+    _run([HIPCC, "-shared"] + HIP_FLAGS + [os.path.join(CSRC, "hbm_probe.hip"), "-o", tmp], verbose)
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 

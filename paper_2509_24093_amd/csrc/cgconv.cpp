@@ -444,6 +444,18 @@ hipError_t alloc_gate_workspace(cgconv_plan* p) {
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+// distinct complex products q[l1,m1] * k[l2,m2] among the contraction terms
+int64_t distinct_products(const std::vector<Term>& terms, int K) {
+  std::vector<char> seen((size_t)K * K, 0);
+  int64_t n = 0;
+  for (const Term& t : terms) {
+    char& f = seen[(size_t)comp(t.l1, t.m1) * K + comp(t.l2, t.m2)];
+    n += f == 0;
+    f = 1;
+  }
+  return n;
+}
+
 // the token-DFT entry points: everything but a graph plan
 int check_forward_args(cgconv_plan* p, const void* q, const void* k, const void* out) {
   const int st = check_plan_args(p, q, k, out);
@@ -569,14 +581,7 @@ cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32
     delete p;
     return nullptr;
   }
-  {
-    std::vector<char> seen((size_t)K * K, 0);
-    for (const Term& t : terms) {
-      char& f = seen[(size_t)comp(t.l1, t.m1) * K + comp(t.l2, t.m2)];
-      p->products += f == 0;
-      f = 1;
-    }
-  }
+  p->products = distinct_products(terms, K);
   p->paths = n_paths(L_max);
   // each workspace holds a [B][N][K][C] float2 array, followed by a trash area
   // that absorbs the masked stores of the CG stage (K*Cp float2, at least 256)
@@ -657,7 +662,11 @@ cgconv_plan_t cgconv_plan_create_graph(int64_t batch, int64_t N, int32_t L_max, 
   p->L = L_max;
   p->K = K;
   p->paths = n_paths(L_max);
-  p->nnz = (int64_t)contraction_terms(L_max).size();
+  {
+    const std::vector<Term> terms = contraction_terms(L_max);
+    p->nnz = (int64_t)terms.size();
+    p->products = distinct_products(terms, K);
+  }
   p->rtable = real_table(L_max);  // the per-frequency product is the generated real-basis body
   p->Kp = round_up(N, 32);
   p->Mp = round_up(N, 128);
