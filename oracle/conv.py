@@ -50,21 +50,18 @@ def _rows_direct(qb, kb, i_list, RK):
     qb, kb: (N, K, C), any float dtype; the sum runs in float64.
     Returns (len(i_list), K, C).
 
-    P_i = sum_j q_j (x) k_{(i-j) mod N} = sum_m q_{(i-m) mod N} (x) k_m.  With
-    qr[t] = q[(-t) mod N] the first factor is qr[(m-i) mod N]; the sum over m
-    is taken in two contiguous ranges, m = i..N-1 (qr[0..N-1-i]) and
-    m = 0..i-1 (qr[N-i..N-1]), each as one matrix product.
+    P_i = sum_j q_j (x) k_{(i-j) mod N}: the keys are gathered at (i - j) mod N
+    for j = 0..N-1, and the sum over j is one matrix product per channel;
+    then u_i = R_full : P_i.
     """
     N, K, C = qb.shape
-    qrT = np.empty((C, K, N))                                   # qr as [c, a, t]
-    qrT[:, :, 0] = qb[0].T
-    qrT[:, :, 1:] = np.transpose(qb[:0:-1], (2, 1, 0))          # q[N-1], ..., q[1]
-    kT = np.ascontiguousarray(np.transpose(kb, (2, 0, 1)), dtype=np.float64)  # k as [c, m, b]
+    qT = np.ascontiguousarray(np.transpose(qb, (2, 1, 0)), dtype=np.float64)   # q as [c, a, j]
+    kT = np.ascontiguousarray(np.transpose(kb, (2, 0, 1)), dtype=np.float64)   # k as [c, m, b]
+    j = np.arange(N)
     out = np.empty((len(i_list), K, C))
     for n, i in enumerate(i_list):
-        P = np.matmul(qrT[:, :, :N - i], kT[:, i:, :])          # m = i .. N-1
-        if i > 0:
-            P += np.matmul(qrT[:, :, N - i:], kT[:, :i, :])     # m = 0 .. i-1
+        ks = kT[:, (i - j) % N, :]                              # [c, j, b] = k[(i-j) mod N, b, c]
+        P = np.matmul(qT, ks)                                   # [c, a, b] = sum_j q[j,a,c] k[(i-j) mod N,b,c]
         out[n] = (P.reshape(C, K * K) @ RK.T).T                 # R_full : P_i for every channel
     return out
 
