@@ -233,6 +233,26 @@ int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const fl
 int cgconv_gate_value(cgconv_plan_t plan, const float* u, const float* v, float* f, hipStream_t stream);
 
 /*
+ * cgconv_gate_value for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same operation and kernels with no plan.  The softmax
+ * partials and statistics live in a library-owned static device array of
+ * 16 MiB, which each device the library runs on holds until the process
+ * ends; this call allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine).  batch, N (tokens), L_max, C: sizes of u, v, f, DEVICE
+ * fp32 [batch][N][(L_max+1)^2][C], 16-byte aligned, f not aliasing u or v;
+ * 1 <= batch <= 65535, N >= 1, 0 <= L_max <= CGCONV_LMAX, C >= 1, and
+ * batch * (ceil(N/64) + 1) * (L_max+1) * C * 8 bytes must fit in the array
+ * (CGCONV_ERR_UNSUPPORTED otherwise; e.g. batch=8, N=16384, L_max=6, C=32
+ * needs 3.7 MB).  Every call on a device shares that device's array: calls
+ * that overlap on one device (two streams, two threads) race and must be
+ * ordered by the caller.  Enqueues on `stream`; the first call on a device
+ * also looks up the array's address there (host-only).
+ */
+int cgconv_gate_value_noalloc(int64_t batch, int64_t N, int32_t L_max, int64_t C, const float* u, const float* v,
+                              float* f, hipStream_t stream);
+
+/*
  * Backward of cgconv_gate_value (the models of §5 are trained through this
  * step too): given grad_f = dL/df, the gradients with respect to u and v by
  * the chain rule through the definition above, with a = g u:

@@ -69,6 +69,8 @@ def library() -> ctypes.CDLL:
     lib.cgconv_backward.restype = ctypes.c_int
     lib.cgconv_gate_value.argtypes = [vp, vp, vp, vp, vp]
     lib.cgconv_gate_value.restype = ctypes.c_int
+    lib.cgconv_gate_value_noalloc.argtypes = [i64, i64, i32, i64, vp, vp, vp, vp]
+    lib.cgconv_gate_value_noalloc.restype = ctypes.c_int
     lib.cgconv_gate_value_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp]
     lib.cgconv_gate_value_backward.restype = ctypes.c_int
     lib.cgconv_paths.argtypes = [i32, ctypes.POINTER(i32), i64]
@@ -165,6 +167,12 @@ def cgconv_backward(plan: int, q: int, k: int, grad_out: int, grad_q, grad_k, st
 def cgconv_gate_value(plan: int, u: int, v: int, f: int, stream: int) -> int:
     """Invariant softmax gating of u and its token-wise CG product with v."""
     return _check(library().cgconv_gate_value(plan, u, v, f, stream))
+
+
+def cgconv_gate_value_noalloc(batch: int, N: int, L_max: int, C: int, u: int, v: int, f: int, stream: int) -> int:
+    """cgconv_gate_value without a plan and without allocation (the library's
+    static device scratch array holds the softmax statistics)."""
+    return _check(library().cgconv_gate_value_noalloc(batch, N, L_max, C, u, v, f, stream))
 
 
 def cgconv_gate_value_backward(plan: int, u: int, v: int, grad_f: int, grad_u, grad_v, stream: int) -> int:

@@ -22,6 +22,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -1226,6 +1227,109 @@ int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, 
   }
   contract_host(L_max, reinterpret_cast<const std::complex<double>*>(qhat),
                 reinterpret_cast<const std::complex<double>*>(khat), reinterpret_cast<std::complex<double>*>(uhat));
+  return CGCONV_OK;
+}
+
+}  // extern "C"
+
+// ---- gating without allocation ---------------------------------------------
+//
+// cgconv_gate_value_noalloc keeps the gating partials and statistics in a
+// file-scope device array instead of a plan workspace.  In host code the
+// array's name is not a device address: its address on each device comes
+// from hipGetSymbolAddress, taken once per device at the entry point's first
+// call there, and only that address is passed to kernels.
+
+namespace {
+
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+__device__ __align__(256) float2 scratch[kNoAllocScratchBytes / sizeof(float2)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+float2* g_scratch_ptr[kMaxDevices] = {};
+
+// this device's copy of the array, or nullptr with the error set
+float2* device_scratch(int dev) {
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      set_error("hipGetSymbolAddress of the gating scratch array failed on device %d: %s", dev,
+                hipGetErrorString(e));
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = static_cast<float2*>(ptr);
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+int cgconv_gate_value_noalloc(int64_t batch, int64_t N, int32_t L_max, int64_t C, const float* u, const float* v,
+                              float* f, hipStream_t stream) {
+  g_last_error.clear();
+  if (batch < 1 || batch > 65535 || N < 1 || C < 1 || L_max < 0) {
+    set_error("invalid sizes: batch=%lld N=%lld L_max=%d C=%lld (need 1 <= batch <= 65535, N >= 1, L_max >= 0, "
+              "C >= 1)", (long long)batch, (long long)N, L_max, (long long)C);
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (L_max > CGCONV_LMAX) {
+    set_error("unsupported L_max=%d: at most %d", L_max, CGCONV_LMAX);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  if (!u || !v || !f) {
+    set_error("u, v and f must be non-NULL device pointers");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!aligned16(u) || !aligned16(v) || !aligned16(f)) {
+    set_error("u, v and f must be 16-byte aligned");
+    return CGCONV_ERR_ALIGNMENT;
+  }
+  if (f == u || f == v) {
+    set_error("f must not alias u or v");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const int K = (L_max + 1) * (L_max + 1);
+  if ((long double)batch * N * K * C > 4.0e9L || N > INT32_MAX || C > INT32_MAX) {
+    set_error("problem too large: batch*N*K*C=%.3Le (max 4e9)", (long double)batch * N * K * C);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  // partials [B][chunks][L+1][C] followed by the statistics [B][L+1][C]
+  const long double chunks = (long double)((N + kGateChunk - 1) / kGateChunk);
+  const long double need = (long double)batch * (L_max + 1) * C * (chunks + 1) * sizeof(float2);
+  if (need > (long double)kNoAllocScratchBytes) {
+    set_error("gating scratch of %.0Lf bytes exceeds the %zu-byte array (batch*(N/64+2)*(L_max+1)*C*8 must fit)",
+              need, kNoAllocScratchBytes);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    set_error("no usable current device (%d): %s", dev, hipGetErrorString(e));
+    return CGCONV_ERR_HIP;
+  }
+  float2* base = device_scratch(dev);
+  if (!base) return CGCONV_ERR_HIP;
+  GateArgs a;
+  a.u = u;
+  a.v = v;
+  a.f = f;
+  a.part = base;
+  a.fin = base + (size_t)batch * (size_t)chunks * (L_max + 1) * C;
+  a.B = (int)batch;
+  a.N = (int)N;
+  a.C = (int)C;
+  a.events = nullptr;
+  e = launch_gate(L_max, a, stream);
+  if (e != hipSuccess) {
+    set_error("kernel launch failed: %s", hipGetErrorString(e));
+    return CGCONV_ERR_HIP;
+  }
   return CGCONV_OK;
 }
 
