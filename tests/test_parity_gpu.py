@@ -138,18 +138,29 @@ def test_table_kernel_matches_generated(L):
 
 
 def test_pointcloud_full_size():
-    """B=8, N=16384, L=6, C=32: whole channels and sampled rows."""
+    """B=8, N=16384, L=6, C=32 in the benchmark's launch configuration: the
+    whole output tensor against the oracle's FFT mode (computed channel by
+    channel), every (batch element, channel) signal within the bar, and
+    sampled rows against the direct definition."""
     name = "pointcloud"
     q, k = _workload(name)
     w = W.WORKLOADS[name]
     got = gpu_forward(q, k, w["L"], tag=name)
-    N = w["N"]
-    for b in (0, 7):
-        chans = [0, 31, 13]
-        ref = cgconv_fft(q[b:b + 1], k[b:b + 1], w["L"], channels=chans)
-        err = rel_l2(got[b:b + 1][..., chans], ref)
-        print(f"  pointcloud b={b} channels {chans}: rel_l2 = {err:.3e}", flush=True)
-        assert err <= TOL_F32
+    B, N, K, C = q.shape
+    num = den = 0.0
+    worst = 0.0
+    for b in range(B):
+        for c in range(C):
+            ref = cgconv_fft(q[b:b + 1], k[b:b + 1], w["L"], channels=[c])
+            d = got[b:b + 1, ..., c:c + 1].astype(np.float64) - ref
+            n2, r2 = float((d * d).sum()), float((ref * ref).sum())
+            num += n2
+            den += r2
+            worst = max(worst, (n2 / r2) ** 0.5)
+    err = (num / den) ** 0.5
+    print(f"  pointcloud whole tensor: rel_l2 = {err:.3e}, worst (b, channel) signal {worst:.3e}", flush=True)
+    assert err <= TOL_F32
+    assert worst <= TOL_F32
     rows = [(0, 0), (7, N - 1), (3, 1234)]
     ref = cgconv_direct_rows(q, k, w["L"], rows)
     for n, (b, i) in enumerate(rows):
@@ -173,11 +184,12 @@ def test_large_full_size(bf16):
         got = gpu_forward(q, k, w["L"], tag=name)
         qr, kr = q, k
         tol = TOL_F32
-    chans = [0, 63]
-    ref = cgconv_fft(qr[1:2], kr[1:2], w["L"], channels=chans)
-    err = rel_l2(got[1:2][..., chans], ref)
-    print(f"  large b=1 channels {chans}: rel_l2 = {err:.3e}", flush=True)
-    assert err <= tol
+    chans = [0, 21, 42, 63] if not bf16 else [0, 63]
+    for b in range(w["B"]):
+        ref = cgconv_fft(qr[b:b + 1], kr[b:b + 1], w["L"], channels=chans)
+        err = rel_l2(got[b:b + 1][..., chans], ref)
+        print(f"  large b={b} channels {chans}: rel_l2 = {err:.3e}", flush=True)
+        assert err <= tol
     rows = [(0, 0), (1, w["N"] - 1)]
     ref = cgconv_direct_rows(qr, kr, w["L"], rows)
     for n, (b, i) in enumerate(rows):
