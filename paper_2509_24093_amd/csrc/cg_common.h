@@ -15,6 +15,8 @@ template <int L>
 struct CgPathBody;  // per-path variant for the channel-mixing kernel (same files)
 template <int L>
 struct CgRealBody;  // token-wise real-basis product of the value tensor product (same files)
+template <int L>
+struct CgSplitBody;  // lane-pair variant: one point per two lanes (same files)
 
 constexpr int kCgThreads = 256;
 
@@ -30,6 +32,23 @@ __device__ __forceinline__ float fnma(float a, float b, float c) {
 // value of the lane with index lane ^ 1 (quad_perm [1,0,3,2])
 __device__ __forceinline__ float swap_pair(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+
+// value of the lane with index lane ^ 1 (a lane-swap move; the lane-pair
+// contraction keeps every lane active).  Written as volatile assembly so
+// that it stays where the generated code puts it, next to the products that
+// use it: as a builtin the compiler hoisted the partner values of a whole
+// phase and spilled them.
+__device__ __forceinline__ float lane_partner(float v) {
+  float r;
+  asm volatile("v_mov_b32_dpp %0, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1" : "=v"(r) : "v"(v));
+  return r;
+}
+__device__ __forceinline__ float2 lane_partner2(float2 v) { return make_float2(lane_partner(v.x), lane_partner(v.y)); }
+
+// value of the lane with index lane ^ 2 (quad_perm [2,3,0,1])
+__device__ __forceinline__ float swap_quad_pair(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, true));
 }
 
 // Branch-free store of one output component of a channel pair.  Control flow
@@ -118,6 +137,89 @@ __device__ __forceinline__ void load_unpack(const CgArgs& a, const Point& pt, Ar
     ka[k] = make_float2(A.y + B.y, B.x - A.x);  // -i (A - conj B)  = 2K
   }
   to_complex_basis<K>(qa, ka);
+}
+
+// Lane-pair form: point p sits on lanes 2p (half 0) and 2p + 1 (half 1);
+// channels c, c + 1 of a channel pair are lanes 4j, 4j+1 and 4j+2, 4j+3.  The
+// even lane of a point holds the output; half 0 of channel c writes row w,
+// half 0 of channel c + 1 row N - w, the odd lanes write into the trash area.
+struct SplitPairStore {
+  float2* dst;
+  int Cp;
+  bool even;  // channel c of the pair
+  __device__ __forceinline__ void operator()(int kout, float2 u) const {
+    const float2 v = make_float2(swap_quad_pair(u.x), swap_quad_pair(u.y));
+    const float2 out = even ? make_float2(u.x - v.y, u.y + v.x) : make_float2(v.x + u.y, u.x - v.y);
+    dst[(long long)kout * Cp] = out;
+  }
+  __device__ __forceinline__ void end_phase(int) const {}
+};
+
+// Lane-pair loads: half 0 of a point reads the spectrum at w, half 1 the
+// one at N-w, and the two lanes swap them; half 0 keeps 2Q, half 1 keeps
+// (-1)^l 2K, in the complex-m basis (the sign commutes with the basis change,
+// which stays within a degree).  Loads run one group of components ahead of
+// their use (compiler memory barriers keep every group's loads together):
+// all K loads up front would need K registers more, and one group at a time
+// waited a full memory round trip per group.
+template <int K, class Arr>
+__device__ __forceinline__ void load_unpack_half(const CgArgs& a, const Point& pt, int half, Arr& x) {
+  const bool cv = pt.valid && pt.c < a.C;
+  const long long wn = (a.N - pt.w) & (a.N - 1);
+  const int cl = pt.c < a.C ? pt.c : a.C - 1;
+  const float2* z = a.Z + ((pt.b * a.N + freq_row(half ? wn : pt.w, a)) * K) * a.C + cl;
+  constexpr int G = 16, NG = (K + G - 1) / G;
+  float2 buf[2][G];
+  auto issue = [&](int g) {
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+      if (g * G + i < K) buf[g & 1][i] = z[(long long)(g * G + i) * a.C];
+  };
+  issue(0);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    if (g + 1 < NG) issue(g + 1);
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      const int k = g * G + i;
+      if (k >= K) break;
+      float2 v = buf[g & 1][i];
+      v.x = cv ? v.x : 0.f;
+      v.y = cv ? v.y : 0.f;
+      const float2 u = lane_partner2(v);
+      const float2 A = half ? u : v, B = half ? v : u;  // spectra at w and N-w
+      int l = 0;
+      while ((l + 1) * (l + 1) <= k) ++l;  // compile-time after unrolling
+      const float sg = (l & 1) ? -1.f : 1.f;
+      x[k] = half ? make_float2(sg * (A.y + B.y), sg * (B.x - A.x)) : make_float2(A.x + B.x, A.y - B.y);
+      // opaque from here on: the compiler may not recompute x[k] from the
+      // loaded values at its uses
+      asm volatile("" : "+v"(x[k].x), "+v"(x[k].y));
+    }
+  }
+#pragma unroll
+  for (int l = 1; l * l < K; ++l) {
+#pragma unroll
+    for (int mu = 1; mu <= l; ++mu) {
+      const int c = l * l + l + mu, sn = l * l + l - mu;
+      const float2 xc = x[c], xs = x[sn];
+      x[sn] = make_float2(xc.x - xs.y, xc.y + xs.x);
+      x[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
+    }
+  }
+}
+
+__device__ __forceinline__ SplitPairStore make_split_store(const CgArgs& a, const Point& pt, int half, int K) {
+  SplitPairStore st;
+  const long long wn = (a.N - pt.w) & (a.N - 1);
+  st.Cp = a.Cp;
+  st.even = (pt.c & 1) == 0;
+  const bool write = half == 0 && pt.valid && (st.even || (wn != pt.w));
+  const long long row = freq_row(st.even ? pt.w : wn, a);
+  float2* real = a.W + ((pt.b * a.N + row) * K) * a.Cp + (pt.c >> 1);
+  st.dst = write ? real : a.trash + (pt.c >> 1);
+  return st;
 }
 
 __device__ __forceinline__ PairStore make_store(const CgArgs& a, const Point& pt, int K) {

@@ -31,12 +31,34 @@ __global__ __launch_bounds__(cgdev::kCgThreads, kMinWavesPerSimd) void cg_gen_ke
   CgBody<L>::run(qa, ka, st);
 }
 
+// L_max 7 and 8: one point per pair of lanes (CgSplitBody), each lane with
+// K instead of 2K input values, so that two waves share a SIMD: a single
+// wave issues at most one instruction every ~4.8 cycles, two waves one every
+// ~2.4, which outweighs the larger operation count of the lane-pair form.
+template <int L>
+__global__ __launch_bounds__(cgdev::kCgThreads, 2) void cg_split_kernel(CgArgs a) {
+  using namespace cgdev;
+  constexpr int K = (L + 1) * (L + 1);
+  const long long lane = (long long)blockIdx.x * kCgThreads + threadIdx.x;
+  const int half = (int)(lane & 1);
+  const Point pt = point_of(lane >> 1, a);
+  float2 x[K];
+  load_unpack_half<K>(a, pt, half, x);
+  SplitPairStore st = make_split_store(a, pt, half, K);
+  CgSplitBody<L>::run(x, st);
+}
+
 }  // namespace
 
 template <>
 hipError_t launch_cg_gen<CGCONV_TU_L>(const CgArgs& a, hipStream_t s) {
-  const long long blocks = (a.npts + cgdev::kCgThreads - 1) / cgdev::kCgThreads;
-  hipLaunchKernelGGL(cg_gen_kernel<CGCONV_TU_L>, dim3((unsigned)blocks), dim3(cgdev::kCgThreads), 0, s, a);
+  if constexpr (CGCONV_TU_L >= 7) {
+    const long long blocks = (2 * a.npts + cgdev::kCgThreads - 1) / cgdev::kCgThreads;
+    hipLaunchKernelGGL(cg_split_kernel<CGCONV_TU_L>, dim3((unsigned)blocks), dim3(cgdev::kCgThreads), 0, s, a);
+  } else {
+    const long long blocks = (a.npts + cgdev::kCgThreads - 1) / cgdev::kCgThreads;
+    hipLaunchKernelGGL(cg_gen_kernel<CGCONV_TU_L>, dim3((unsigned)blocks), dim3(cgdev::kCgThreads), 0, s, a);
+  }
   return hipGetLastError();
 }
 

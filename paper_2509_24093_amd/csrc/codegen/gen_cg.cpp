@@ -454,6 +454,121 @@ void emit_path_body(FILE* f, int L, long* ops_out) {
   *ops_out = ops;
 }
 
+// Lane-pair body for L_max 7 and 8 (CgSplitBody<L>::run(x, st)): one point
+// per pair of adjacent lanes, so that a lane holds K instead of 2K input
+// values and two waves fit on a SIMD.  The even lane holds x = qa, the odd
+// lane x[(l,m)] = (-1)^l ka[(l,m)], both in the complex-m basis.  For an
+// unordered component pair {o, q} one product p = x[o] * partner(x[q]) gives
+// the even lane (-1)^l_q qa[o] ka[q] (the term (o, q)) and the odd lane
+// (-1)^l_o qa[q] ka[o] (the term (q, o)).  Both lanes take the coefficient
+// (-1)^l_q c(o, q, J); by the swap symmetry c(q, o, J) =
+// (-1)^(l_o + l_q - J) c(o, q, J) the odd lane's sum is then (-1)^J times its
+// share of w[J, M], so w = acc + (-1)^J partner(acc) in the even lane.  A
+// diagonal pair (o == q) has terms of even J only and takes half its
+// coefficient in each lane.  Products are grouped by their partner factor,
+// fetched once per group (two lane-swap moves).  Per lane this is about
+// 2/3 of the single-lane body's operations, at half the registers.
+void emit_split_body(FILE* f, int L, long* ops_out) {
+  const int K = (L + 1) * (L + 1);
+  std::vector<Term> terms = contraction_terms(L);
+  TermMap terms_of;
+  for (const Term& t : terms) terms_of[{t.l1, t.m1, t.l2, t.m2}].push_back(t);
+  L_cur = L;
+  auto lm = [](int c, int& l, int& m) {
+    l = 0;
+    while ((l + 1) * (l + 1) <= c) ++l;
+    m = c - l * l - l;
+  };
+  Emitter e{f, {}, 0};
+  std::fprintf(f, "template <>\nstruct CgSplitBody<%d> {\n  static constexpr int K = %d;\n", L, K);
+  std::fprintf(f, "  template <class Store>\n");
+  std::fprintf(f, "  static __device__ __forceinline__ void run(const float2 (&x)[%d], Store& st) {\n", K);
+  for (int mu = 0; mu <= L; ++mu) {
+    std::fprintf(f, "    {  // phase |M| = %d\n", mu);
+    std::vector<int> Ms = mu == 0 ? std::vector<int>{0} : std::vector<int>{mu, -mu};
+    for (int M : Ms)
+      for (int J = mu; J <= L; ++J) std::fprintf(f, "      float2 %s;\n", acc_name(M, J).c_str());
+    // unordered pairs {o < q} and diagonals of this phase, grouped by q
+    std::map<int, std::vector<int>> groups;
+    for (const auto& kv : terms_of) {
+      const int o = comp(kv.first[0], kv.first[1]), q = comp(kv.first[2], kv.first[3]);
+      const int M = kv.first[1] + kv.first[3];
+      if (std::find(Ms.begin(), Ms.end(), M) == Ms.end() || o > q) continue;
+      if (o != q) {
+        auto it = terms_of.find({kv.first[2], kv.first[3], kv.first[0], kv.first[1]});
+        if (it == terms_of.end() || it->second.size() != kv.second.size()) {
+          std::fprintf(stderr, "gen_cg: swap partner missing (split body)\n");
+          std::exit(1);
+        }
+        for (const Term& t : kv.second) {
+          const Term* u = nullptr;
+          for (const Term& w : it->second)
+            if (w.J == t.J) u = &w;
+          const double sigma = ((t.l1 + t.l2 - t.J) % 2 == 0) ? 1.0 : -1.0;
+          if (!u || u->imag != t.imag || std::fabs(u->coef - sigma * t.coef) > 1e-12 * std::fabs(t.coef) + 1e-15) {
+            std::fprintf(stderr, "gen_cg: swap symmetry violated (split body)\n");
+            std::exit(1);
+          }
+        }
+      } else {
+        for (const Term& t : kv.second)
+          if (t.J % 2 != 0) {
+            std::fprintf(stderr, "gen_cg: diagonal term of odd J (split body)\n");
+            std::exit(1);
+          }
+      }
+      groups[q].push_back(o);
+    }
+    for (const auto& g : groups) {
+      const int q = g.first;
+      int lq, mq;
+      lm(q, lq, mq);
+      std::fprintf(f, "      { const float2 pq = lane_partner2(x[%d]);\n", q);
+      e.ops += 2;
+      for (int o : g.second) {
+        int lo, mo;
+        lm(o, lo, mo);
+        std::fprintf(f, "      { const float pr = fnma(x[%d].y, pq.y, x[%d].x * pq.x);", o, o);
+        std::fprintf(f, " const float pi = fmaf(x[%d].y, pq.x, x[%d].x * pq.y);\n", o, o);
+        e.ops += 4;
+        const double scale = ((lq % 2) ? -1.0 : 1.0) * (o == q ? 0.5 : 1.0);
+        for (const Term& t : terms_of.at({lo, mo, lq, mq}))
+          e.acc_add_scaled(acc_name(t.M, t.J), scale * t.coef, t.imag, "pr", "pi");
+        std::fprintf(f, "      }\n");
+      }
+      std::fprintf(f, "      }\n");
+      std::fprintf(f, "      __builtin_amdgcn_sched_barrier(0);\n");
+    }
+    // the even lane's w = acc + (-1)^J partner(acc), then the real basis
+    for (int J = mu; J <= L; ++J) {
+      for (int M : Ms) {
+        const std::string a = acc_name(M, J);
+        if (!e.inited.count(a)) std::fprintf(f, "      %s = make_float2(0.f, 0.f);\n", a.c_str());
+        const char* op = J % 2 ? "-" : "+";
+        std::fprintf(f, "      %s.x = %s.x %s lane_partner(%s.x); %s.y = %s.y %s lane_partner(%s.y);\n", a.c_str(),
+                     a.c_str(), op, a.c_str(), a.c_str(), a.c_str(), op, a.c_str());
+        e.ops += 2;
+      }
+      if (mu == 0) {
+        std::fprintf(f, "      st(%d, %s);\n", comp(J, 0), acc_name(0, J).c_str());
+      } else {
+        const std::string p = acc_name(mu, J), m = acc_name(-mu, J);
+        std::fprintf(f, "      st(%d, make_float2(%s.x + %s.x, %s.y + %s.y));\n", comp(J, mu), m.c_str(),
+                     p.c_str(), m.c_str(), p.c_str());
+        std::fprintf(f, "      st(%d, make_float2(%s.y - %s.y, %s.x - %s.x));\n", comp(J, -mu), m.c_str(),
+                     p.c_str(), p.c_str(), m.c_str());
+        e.ops += 4;
+      }
+    }
+    e.inited.clear();
+    std::fprintf(f, "      st.end_phase(%d);\n", mu);
+    std::fprintf(f, "    }\n");
+  }
+  std::fprintf(f, "  }\n");
+  std::fprintf(f, "  static constexpr long kOps = %ld;  // VALU ops per lane (two lanes per point)\n};\n\n", e.ops);
+  *ops_out = e.ops;
+}
+
 // Token-wise real-basis product for the value tensor product (CgRealBody<L>::run):
 //   f[J,M] = sum R^{(l1 l2 J)}[M,m1,m2] a[l1,m1] b[l2,m2]   (a, b, f real)
 // from the real-basis table.  The two ordered terms of a component pair
@@ -546,13 +661,15 @@ int main(int argc, char** argv) {
     }
     std::fprintf(f, "// Generated by csrc/codegen/gen_cg.cpp -- do not edit.\n");
     std::fprintf(f, "// Frequency-domain CG contraction body, L_max = %d.\n#pragma once\n\n", L);
-    long ops = 0, pops = 0, rops = 0;
+    long ops = 0, pops = 0, rops = 0, sops = 0;
     emit_body(f, L, &ops);
     emit_path_body(f, L, &pops);
     emit_real_body(f, L, &rops);
+    emit_split_body(f, L, &sops);
     std::fclose(f);
-    std::fprintf(stderr, "gen_cg: L=%d ops/point=%ld per-path ops/point=%ld real token-wise ops=%ld\n", L, ops,
-                 pops, rops);
+    std::fprintf(stderr,
+                 "gen_cg: L=%d ops/point=%ld per-path ops/point=%ld real token-wise ops=%ld lane-pair ops/lane=%ld\n",
+                 L, ops, pops, rops, sops);
   }
   const std::string hpath = dir + "/cg_lgen.h";
   FILE* h = std::fopen(hpath.c_str(), "w");
