@@ -296,7 +296,7 @@ def cg_roofline(stage_avg, B, N, L, C, n_products, nnz, traffic, traffic_src):
         flop_model += f" + {dft}-flop length-64 DFTs on {B * n1 * K * (C + Cp)} columns"
     achieved_tflops = flops / (cg_ms * 1e-3) / 1e12
     return {
-        "kernel": f"{'cg_fused_kernel' if dom == 'cg_fused' else 'cg_gen_kernel'}<{L}>",
+        "kernel": f"{'cg_fused_kernel' if dom == 'cg_fused' else ('cg_split_kernel' if L >= 7 else 'cg_gen_kernel')}<{L}>",
         "bound": "alu",
         "achieved": round(achieved_tflops, 2),
         "peak": round(VALU_PEAK_TFLOPS, 1),

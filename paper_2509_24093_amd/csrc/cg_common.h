@@ -168,23 +168,26 @@ __device__ __forceinline__ void load_unpack_half(const CgArgs& a, const Point& p
   const long long wn = (a.N - pt.w) & (a.N - 1);
   const int cl = pt.c < a.C ? pt.c : a.C - 1;
   const float2* z = a.Z + ((pt.b * a.N + freq_row(half ? wn : pt.w, a)) * K) * a.C + cl;
-  constexpr int G = 16, NG = (K + G - 1) / G;
-  float2 buf[2][G];
+  // (groups of 8 with two or three in flight, or of 16 or 32 with one or
+  // two, measured the same or slower at L_max = 8)
+  constexpr int G = 16, D = 1, NG = (K + G - 1) / G;
+  float2 buf[D + 1][G];
   auto issue = [&](int g) {
 #pragma unroll
     for (int i = 0; i < G; ++i)
-      if (g * G + i < K) buf[g & 1][i] = z[(long long)(g * G + i) * a.C];
+      if (g * G + i < K) buf[g % (D + 1)][i] = z[(long long)(g * G + i) * a.C];
   };
-  issue(0);
+#pragma unroll
+  for (int g = 0; g < D && g < NG; ++g) issue(g);
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
-    if (g + 1 < NG) issue(g + 1);
+    if (g + D < NG) issue(g + D);
     asm volatile("" ::: "memory");
 #pragma unroll
     for (int i = 0; i < G; ++i) {
       const int k = g * G + i;
       if (k >= K) break;
-      float2 v = buf[g & 1][i];
+      float2 v = buf[g % (D + 1)][i];
       v.x = cv ? v.x : 0.f;
       v.y = cv ? v.y : 0.f;
       const float2 u = lane_partner2(v);
