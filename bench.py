@@ -54,6 +54,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 VALU_PEAK_TFLOPS = 256 * 4 * 32 * 2 * 2.4e9 / 1e12
 METRIC = "CG-conv tokens/sec at N=16384, L_max=6, C=32; achieved HBM GB/s vs peak"
 METRIC_MIXED = "CG-conv with per-path channel mixing, tokens/sec at N=16384, L_max=6, C=32"
+METRIC_INTER = ("inter-channel CG-conv (4 heads x 8 channels, all channel pairs, per-degree reduction to 8), "
+                "tokens/sec at N=16384, L_max=6")
 METRIC_GRAPH = "CG-conv in a graph Fourier basis, tokens/sec at N=4096, L_max=6, C=32"
 METRIC_LINEAR = "CG-conv with the zero-padded (linear) boundary, tokens/sec at N=16384, L_max=6, C=32"
 METRIC_BACKWARD = "CG-conv backward (grad_q and grad_k), tokens/sec at N=16384, L_max=6, C=32"
@@ -321,6 +323,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--mixed", action="store_true")
+    ap.add_argument("--interchannel", action="store_true")
+    ap.add_argument("--heads", type=int, default=4)
     ap.add_argument("--backward", action="store_true")
     ap.add_argument("--gate", action="store_true")
     ap.add_argument("--gate-backward", action="store_true")
@@ -366,6 +370,9 @@ def main():
     plan = P.Plan(B, N, L, C, boundary=args.boundary)
     if args.mixed:
         bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C)
+        return
+    if args.interchannel:
+        bench_interchannel(args, plan, q, k, qd, kd, B, N, L, C)
         return
     if args.backward:
         bench_backward(args, plan, q, k, qd, kd, B, N, L, C)
@@ -542,6 +549,78 @@ def bench_mixed(args, plan, q, k, qd, kd, out, B, N, L, C):
                                             f"rows (b, i), fp64 numpy, {dt:.1f} s"}
         result["parity_rel_l2_sampled_rows"] = (num / den) ** 0.5
         log(f"[bench] mixed parity on {len(rows)} rows: rel_l2 = {result['parity_rel_l2_sampled_rows']:.3e}")
+    else:
+        result["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(result), flush=True)
+
+
+def bench_interchannel(args, plan, q, k, qd, kd, B, N, L, C):
+    """cgconv_forward_interchannel with H heads of m = C/H channels, every
+    channel pair of a head, reduced per degree to m_out = m channels by
+    seeded weights ~ N(0, 1/m^2)."""
+    import numpy as np
+    import torch
+
+    H = args.heads
+    m = C // H
+    mo = m
+    wts = (np.random.default_rng(2031).normal(size=(H, L + 1, mo, m * m)) / m).astype(np.float32)
+    wd = torch.from_numpy(wts).cuda()
+    out = torch.empty((B, N, (L + 1) ** 2, H * mo), dtype=torch.float32, device="cuda")
+    log(f"[bench] timing {args.steps} inter-channel steps (heads {H}, m {m}, m_out {mo})")
+    ms, stage_avg, timing = _timed(args, lambda: plan.forward_interchannel(qd, kd, wd, heads=H, out=out), plan)
+    nnz, n_products = plan.contraction_info()
+    F = N // 2 + 1
+    pts = B * F * H * 64                       # lanes: (point, pair slot); m*m of 64 slots carry pairs
+    pair_pts = B * F * H * m * m
+    cg_flops = pair_pts * (6 * n_products + 4 * nnz)
+    mfma_flops = B * H * ((F + 3) // 4) * sum(2 * 16 * 16 * 64 * (1 if mu == 0 else 1) * (L + 1 - mu)
+                                              for mu in range(L + 1))
+    ims = stage_avg["cg_inter"]
+    achieved = cg_flops / (ims * 1e-3) / 1e12
+    result = _common(args, METRIC_INTER, ms, B, N, L, C, "f32 (reduction: fp32 MFMA)", timing)
+    result["config"].update({"heads": H, "channels_per_head": m, "m_out": mo, "weights": "N(0, 1/m^2), seed 2031"})
+    result["roofline"] = {
+        "kernel": f"cg_inter_kernel<{L}>",
+        "bound": "alu",
+        "achieved": round(achieved, 2),
+        "peak": round(VALU_PEAK_TFLOPS, 1),
+        "unit": "TFLOP/s",
+        "frac": round(achieved / VALU_PEAK_TFLOPS, 4),
+        "traffic": None,
+        "flops_per_launch": cg_flops,
+        "flop_model": (f"(6*{n_products} distinct complex products + 4*{nnz} non-zeros) per (b, frequency 0..N/2, "
+                       f"head, channel pair) point, {pair_pts} points; the per-degree reduction runs on the matrix "
+                       f"cores: {mfma_flops} fp32 MFMA flops per launch (16x16x4, rows padded to 16)"),
+        "reduction_mfma_tflops": round(mfma_flops / (ims * 1e-3) / 1e12, 2),
+        "launch_ms": round(ims, 4),
+    }
+    result["stages"] = {s: {"ms": round(t, 4)} for s, t in stage_avg.items()}
+    if not args.no_cpu_baseline and args.boundary == "cyclic":
+        from oracle.conv import cgconv_direct_rows
+        from oracle.inter import pair_channels, reduce_degrees
+        log(f"[bench] CPU oracle baseline, inter-channel (~{args.cpu_seconds:.0f} s)")
+        got = out.cpu().numpy()
+        rng = np.random.default_rng(2032)
+        rows, num, den = 0, 0.0, 0.0
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_seconds or rows < 2:
+            b, i = (0, 0) if rows == 0 else (int(rng.integers(0, B)), int(rng.integers(0, N)))
+            qe, ke = pair_channels(q[b:b + 1], k[b:b + 1], H)
+            u = cgconv_direct_rows(qe, ke, L, [(0, i)])          # (1, K, H m^2)
+            ref = reduce_degrees(u[None], L, H, wts)[0, 0]      # (K, H m_out)
+            d = got[b, i].astype(np.float64) - ref
+            num += float((d * d).sum())
+            den += float((ref * ref).sum())
+            rows += 1
+        dt = time.perf_counter() - t0
+        cores = len(os.sched_getaffinity(0))
+        result["cpu_baseline"] = {"value": rows / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+                                  "sample": f"direct definition over every channel pair with the per-degree "
+                                            f"reduction, {rows} sampled output rows (b, i), fp64 numpy, {dt:.1f} s"}
+        result["parity_rel_l2_sampled_rows"] = (num / den) ** 0.5
+        log(f"[bench] inter-channel parity on {rows} rows: rel_l2 = {result['parity_rel_l2_sampled_rows']:.3e}")
     else:
         result["cpu_baseline"] = None
     plan.close()

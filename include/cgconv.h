@@ -151,6 +151,31 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
                          float* out, hipStream_t stream);
 
 /*
+ * Inter-channel CG convolution with a per-degree channel reduction (§4.1:
+ * query features with m channels and key features with m' channels give a
+ * product with (2J+1) m m' components per degree, heads do not interact, and
+ * the multiplicity is reduced again by a learned equivariant map, read here
+ * as one real matrix per head and output degree):
+ *
+ *   out[b,i,(J,M),h*m_out+o] = sum_{c1,c2} weights[h][J][o][c1*m+c2]
+ *        * sum_paths sum R^{(l1 l2 J)}[M,m1,m2]
+ *          * sum_j q[b,j,(l1,m1),h*m+c1] * k[b,(i-j) mod N,(l2,m2),h*m+c2]
+ *
+ * with the plan's C = heads * m channels in heads of m (channel c = h*m + c'),
+ * and its token boundary.  q, k: DEVICE fp32 [batch][N][(L_max+1)^2][C];
+ * weights: DEVICE fp32 [heads][L_max+1][m_out][m*m], 16-byte aligned;
+ * out: DEVICE fp32 [batch][N][(L_max+1)^2][heads*m_out], not aliasing q, k or
+ * weights.  Needs L_max <= 6, m <= 8, m_out even and <= m
+ * (CGCONV_ERR_UNSUPPORTED otherwise; heads must divide C).  Every channel
+ * pair's product is evaluated by the generated contraction on the vector
+ * units and reduced per degree on the matrix cores (fp32
+ * v_mfma_f32_16x16x4f32), between the unfused FFT passes.  Same stream and
+ * workspace rules as cgconv_forward; the weights are read during the call.
+ */
+int cgconv_forward_interchannel(cgconv_plan_t plan, int32_t heads, int32_t m_out, const float* q, const float* k,
+                                const float* weights, float* out, hipStream_t stream);
+
+/*
  * CG convolution in a graph Fourier basis (appendix "Fourier Space
  * Attention": the eigenvectors U of a graph's normalised Laplacian define the
  * transform x_hat = U^T x, inverse x = U x_hat, and a spectral convolution
@@ -351,7 +376,8 @@ int cgconv_contract_host(int32_t L_max, const double* qhat, const double* khat, 
  * fft_inv_2; for plans with 512 <= N <= 32768 and L_max <= 6: fft_fwd_1,
  * cg_fused, fft_inv_2) and the number of timed calls.  The first timed call
  * fixes which kind is timed: plain forwards, mixed forwards (cg_mix replaces
- * cg and the unfused passes are listed), backwards (each of the two
+ * cg and the unfused passes are listed), inter-channel forwards (cg_inter
+ * likewise), backwards (each of the two
  * gradients is one timed call with the plain stages), gating calls
  * (gate_partials, gate_finalize, gate_value), gating backwards (gate_stats,
  * gate_bwd, gate_sums, gate_bwd_du) or graph forwards

@@ -65,6 +65,8 @@ def library() -> ctypes.CDLL:
     lib.cgconv_forward_bf16.restype = ctypes.c_int
     lib.cgconv_forward_mixed.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.cgconv_forward_mixed.restype = ctypes.c_int
+    lib.cgconv_forward_interchannel.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp]
+    lib.cgconv_forward_interchannel.restype = ctypes.c_int
     lib.cgconv_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp]
     lib.cgconv_backward.restype = ctypes.c_int
     lib.cgconv_gate_value.argtypes = [vp, vp, vp, vp, vp]
@@ -156,6 +158,13 @@ def cgconv_forward_bf16(plan: int, q: int, k: int, out: int, stream: int) -> int
 def cgconv_forward_mixed(plan: int, q: int, k: int, weights: int, out: int, stream: int) -> int:
     """Per-path channel mixing; weights: device fp32 [n_paths][C][C]."""
     return _check(library().cgconv_forward_mixed(plan, q, k, weights, out, stream))
+
+
+def cgconv_forward_interchannel(plan: int, heads: int, m_out: int, q: int, k: int, weights: int, out: int,
+                                stream: int) -> int:
+    """Inter-channel product reduced per degree; weights: device fp32
+    [heads][L_max+1][m_out][m*m], out: [batch, N, K, heads*m_out]."""
+    return _check(library().cgconv_forward_interchannel(plan, heads, m_out, q, k, weights, out, stream))
 
 
 def cgconv_backward(plan: int, q: int, k: int, grad_out: int, grad_q, grad_k, stream: int) -> int:
@@ -338,6 +347,34 @@ class Plan:
                 or tuple(weights.shape) != (P, C, C) or not weights.is_contiguous()):
             raise ValueError(f"weights must be a contiguous float32 GPU tensor of shape {(P, C, C)}")
         cgconv_forward_mixed(self._h, q.data_ptr(), k.data_ptr(), weights.data_ptr(), out.data_ptr(), s)
+        return out
+
+    def forward_interchannel(self, q, k, weights, heads: int, out=None):
+        """Inter-channel product of every channel pair of each head, reduced
+        per output degree (fp32): weights [heads, L_max+1, m_out, m*m] with
+        m = C // heads; returns [batch, N, K, heads*m_out]."""
+        import torch
+        B, N, K, C = self.shape
+        if not isinstance(weights, torch.Tensor) or weights.ndim != 4 or not weights.is_cuda:
+            raise ValueError("weights must be a GPU tensor of shape [heads, L_max+1, m_out, m*m]")
+        m_out = int(weights.shape[2])
+        m = C // int(heads) if heads else 0
+        if (weights.dtype != torch.float32 or not weights.is_contiguous()
+                or tuple(weights.shape) != (int(heads), self.L_max + 1, m_out, m * m)):
+            raise ValueError(f"weights must be a contiguous float32 tensor of shape "
+                             f"{(int(heads), self.L_max + 1, m_out, m * m)}")
+        if out is None:
+            out = torch.empty((B, N, K, int(heads) * m_out), dtype=torch.float32, device=q.device)
+        for name, t in (("q", q), ("k", k)):
+            if not isinstance(t, torch.Tensor) or not t.is_cuda or tuple(t.shape) != self.shape \
+                    or t.dtype != torch.float32 or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous float32 GPU tensor of shape {self.shape}")
+        if (not out.is_cuda or tuple(out.shape) != (B, N, K, int(heads) * m_out) or out.dtype != torch.float32
+                or not out.is_contiguous()):
+            raise ValueError(f"out must be a contiguous float32 GPU tensor of shape {(B, N, K, int(heads) * m_out)}")
+        s = torch.cuda.current_stream().cuda_stream
+        cgconv_forward_interchannel(self._h, int(heads), m_out, q.data_ptr(), k.data_ptr(), weights.data_ptr(),
+                                    out.data_ptr(), s)
         return out
 
     def gate_value(self, u, v, out=None):

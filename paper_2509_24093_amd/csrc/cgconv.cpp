@@ -130,6 +130,8 @@ const char* const kStagesM2[] = {"fft_fwd_1", "fft_fwd_2", "cg_mix", "fft_inv_1"
 const char* const kStagesM1[] = {"fft_fwd", "cg_mix", "fft_inv"};
 const char* const kStagesG[] = {"gate_partials", "gate_finalize", "gate_value"};
 const char* const kStagesGB[] = {"gate_stats", "gate_bwd", "gate_sums", "gate_bwd_du"};
+const char* const kStagesI2[] = {"fft_fwd_1", "fft_fwd_2", "cg_inter", "fft_inv_1", "fft_inv_2"};
+const char* const kStagesI1[] = {"fft_fwd", "cg_inter", "fft_inv"};
 const char* const kStagesGft[] = {"gft_split_u", "gft_split_x", "gft_gemm_fwd", "gft_product", "gft_split_uhat",
                                   "gft_gemm_inv"};
 // timing kinds: 0 forward, 1 mixed forward, 2 backward (each gradient one call), 3 gating, 4 graph forward,
@@ -137,6 +139,7 @@ const char* const kStagesGft[] = {"gft_split_u", "gft_split_x", "gft_gemm_fwd", 
 constexpr int kKindGate = 3;
 constexpr int kKindGateBwd = 5;
 constexpr int kKindGraph = 4;
+constexpr int kKindInter = 6;
 constexpr int kMaxEvents = 8;  // stages + 1 of the longest pipeline
 
 hipError_t launch_product(int L, const GftProductArgs& a, hipStream_t s) {
@@ -193,6 +196,19 @@ hipError_t launch_mix(int L, const CgArgs& a, hipStream_t s) {
     case 4: return launch_cg_mix<4>(a, s);
     case 5: return launch_cg_mix<5>(a, s);
     case 6: return launch_cg_mix<6>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_inter(int L, const InterArgs& a, hipStream_t s) {
+  switch (L) {
+    case 0: return launch_cg_inter<0>(a, s);
+    case 1: return launch_cg_inter<1>(a, s);
+    case 2: return launch_cg_inter<2>(a, s);
+    case 3: return launch_cg_inter<3>(a, s);
+    case 4: return launch_cg_inter<4>(a, s);
+    case 5: return launch_cg_inter<5>(a, s);
+    case 6: return launch_cg_inter<6>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -371,6 +387,119 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     e = pass(N1, IN_COMPLEX, out_split, 1, N2, p->ws2, nullptr, out, N * Ww, Nu * K * p->C, (int)Ww, 1, N2, 1, N2, 0,
              inv_n);
     if (e != hipSuccess) goto fail;
+    mark();
+  }
+  return CGCONV_OK;
+fail:
+  set_error("kernel launch failed: %s", hipGetErrorString(e));
+  return CGCONV_ERR_HIP;
+}
+
+// Inter-channel convolution with the per-degree reduction: the unfused
+// forward passes over the C input channels, the inter-channel stage (Z ->
+// packed output spectra of H*mo channels), the unfused inverse passes over
+// the output channels.  The output spectra (B*N*K*H*mo/2 complex) fit in a
+// workspace sized for C >= H*mo channels.
+int run_interchannel(cgconv_plan* p, int heads, int mo, const float* q, const float* k, const float* wt, float* out,
+                     hipStream_t s) {
+  const int K = p->K;
+  const int Co = heads * mo, Cpo = Co / 2;
+  const long long Wz = (long long)K * p->C, Wo = (long long)K * Cpo;
+  const long long N = p->N, Nu = p->Nu;
+  const int in_pair = IN_PAIR_F32 + (p->linear ? 3 : 0);
+  auto pass = [&](int R, int inm, int outm, int dir, int groups, const void* in0, const void* in1, void* o,
+                  long long ib, long long ob, int W, int gs_in, int es_in, int gs_out, int fs_out, int inter,
+                  float scale, bool output_side) {
+    PassDesc d;
+    d.R = R;
+    d.in_mode = inm;
+    d.out_mode = outm;
+    d.dir = dir;
+    d.groups = groups;
+    d.batch = (int)p->B;
+    d.a = base_args(p);
+    if (output_side) {  // the inverse passes carry the H*mo output channels
+      d.a.C = Co;
+      d.a.Cp = Cpo;
+      d.a.KC = K * Co;
+    }
+    d.a.in0 = in0;
+    d.a.in1 = in1;
+    d.a.out = o;
+    d.a.in_bstride = ib;
+    d.a.out_bstride = ob;
+    d.a.W = W;
+    d.a.gs_in = gs_in;
+    d.a.es_in = es_in;
+    d.a.gs_out = gs_out;
+    d.a.fs_out = fs_out;
+    d.a.tw_stride = (int)(p->N / R);
+    d.a.inter = inter;
+    d.a.scale = scale;
+    return launch_fft_pass(d, s);
+  };
+  hipEvent_t* ev = nullptr;
+  if (p->timing_calls < p->timing_max && (p->timing_kind < 0 || p->timing_kind == kKindInter)) {
+    p->timing_kind = kKindInter;
+    ev = &p->events[(size_t)p->timing_calls * kMaxEvents];
+    ++p->timing_calls;
+  }
+  int stage = 0;
+  auto mark = [&]() {
+    if (ev) (void)hipEventRecord(ev[stage], s);
+    ++stage;
+  };
+  InterArgs ia;
+  ia.wt = wt;
+  ia.N = N;
+  ia.F = (int)(N / 2 + 1);
+  ia.B = (int)p->B;
+  ia.C = (int)p->C;
+  ia.H = heads;
+  ia.m = (int)(p->C / heads);
+  ia.mo = mo;
+  ia.Cpo = Cpo;
+  const float inv_n = 1.0f / (float)N;
+  hipError_t e;
+  mark();
+  if (p->N1 == 0) {
+    if ((e = pass((int)N, in_pair, OUT_COMPLEX, -1, 1, q, k, p->ws1, Nu * Wz, N * Wz, (int)Wz, 0, 1, 0, 1, 0, 1.0f,
+                  false)) != hipSuccess)
+      goto fail;
+    mark();
+    ia.Z = p->ws1;
+    ia.W = p->ws2;
+    ia.n1_log2 = ilog2(N);
+    ia.n2_log2 = 0;
+    if ((e = launch_inter(p->L, ia, s)) != hipSuccess) goto fail;
+    mark();
+    if ((e = pass((int)N, IN_COMPLEX, OUT_SPLIT_F32, 1, 1, p->ws2, nullptr, out, N * Wo, Nu * K * Co, (int)Wo, 0, 1,
+                  0, 1, 0, inv_n, true)) != hipSuccess)
+      goto fail;
+    mark();
+  } else {
+    const int N1 = (int)p->N1, N2 = (int)p->N2;
+    if ((e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, Nu * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f,
+                  false)) != hipSuccess)
+      goto fail;
+    mark();
+    if ((e = pass(N2, IN_COMPLEX, OUT_COMPLEX, -1, N1, p->ws1, nullptr, p->ws2, N * Wz, N * Wz, (int)Wz, N2, 1, N2, 1,
+                  0, 1.0f, false)) != hipSuccess)
+      goto fail;
+    mark();
+    ia.Z = p->ws2;
+    ia.W = p->ws1;
+    ia.n1_log2 = ilog2(N1);
+    ia.n2_log2 = ilog2(N2);
+    if ((e = launch_inter(p->L, ia, s)) != hipSuccess) goto fail;
+    mark();
+    if ((e = pass(N2, IN_COMPLEX, OUT_COMPLEX, 1, N1, p->ws1, nullptr, p->ws2, N * Wo, N * Wo, (int)Wo, N2, 1, N2, 1,
+                  1, 1.0f, true)) != hipSuccess)
+      goto fail;
+    mark();
+    if ((e = pass(N1, IN_COMPLEX, OUT_SPLIT_F32, 1, N2, p->ws2, nullptr, out, N * Wo, Nu * K * Co, (int)Wo, 1, N2, 1,
+                  N2, 0, inv_n, true)) != hipSuccess)
+      goto fail;
     mark();
   }
   return CGCONV_OK;
@@ -967,7 +1096,7 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
     set_error("plan is NULL or ms is NULL");
     return CGCONV_ERR_INVALID_ARG;
   }
-  const int ns = plan->timing_kind == 1           ? plan->n_stages_mix
+  const int ns = plan->timing_kind == 1 || plan->timing_kind == kKindInter ? plan->n_stages_mix
                  : plan->timing_kind == kKindGate  ? 3
                  : plan->timing_kind == kKindGateBwd ? 4
                  : plan->timing_kind == kKindGraph ? 6
@@ -1004,6 +1133,10 @@ const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
   if (plan->timing_kind == kKindGate) return stage < 3 ? kStagesG[stage] : "";
   if (plan->timing_kind == kKindGateBwd) return stage < 4 ? kStagesGB[stage] : "";
   if (plan->timing_kind == kKindGraph) return stage < 6 ? kStagesGft[stage] : "";
+  if (plan->timing_kind == kKindInter) {
+    if (stage >= plan->n_stages_mix) return "";
+    return plan->N1 ? kStagesI2[stage] : kStagesI1[stage];
+  }
   if (stage >= plan->n_stages) return "";
   if (plan->fused) return kStagesF[stage];
   return plan->N1 ? kStages2[stage] : kStages1[stage];
@@ -1040,6 +1173,37 @@ int cgconv_forward_mixed(cgconv_plan_t plan, const float* q, const float* k, con
     return CGCONV_ERR_UNSUPPORTED;
   }
   return run_forward(plan, q, k, out, false, stream, weights);
+}
+
+int cgconv_forward_interchannel(cgconv_plan_t plan, int32_t heads, int32_t m_out, const float* q, const float* k,
+                                const float* weights, float* out, hipStream_t stream) {
+  const int st = check_forward_args(plan, q, k, out);
+  if (st != CGCONV_OK) return st;
+  if (!weights) {
+    set_error("weights must be a non-NULL device pointer");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (!aligned16(weights)) {
+    set_error("weights must be 16-byte aligned");
+    return CGCONV_ERR_ALIGNMENT;
+  }
+  if (weights == out) {
+    set_error("out must not alias the weights");
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  if (heads < 1 || plan->C % heads != 0 || m_out < 1) {
+    set_error("invalid heads=%d or m_out=%d for C=%lld (heads must divide C, m_out >= 1)", heads, m_out,
+              (long long)plan->C);
+    return CGCONV_ERR_INVALID_ARG;
+  }
+  const int m = (int)(plan->C / heads);
+  if (plan->L > kInterLmax || m > kInterMmax || m_out > m || (m_out & 1)) {
+    set_error("unsupported inter-channel shape: needs L_max <= %d (plan: %d), m = C/heads <= %d (%d), m_out even and "
+              "<= m (%d)",
+              kInterLmax, plan->L, kInterMmax, m, m_out);
+    return CGCONV_ERR_UNSUPPORTED;
+  }
+  return run_interchannel(plan, heads, m_out, q, k, weights, out, stream);
 }
 
 int cgconv_backward(cgconv_plan_t plan, const float* q, const float* k, const float* grad_out, float* grad_q,

@@ -112,6 +112,26 @@ constexpr int kMixCmax = 32;
 // order above (4 KiB per path), zero outside C x C.
 hipError_t launch_prepare_mix_weights(const float* W, uint16_t* wt, int paths, int C, hipStream_t s);
 
+// Inter-channel CG stage with a per-degree channel reduction (cg_inter.hip),
+// one specialisation per L_max <= kInterLmax: for every frequency point w in
+// [0, N/2] of batch element b and head h, every channel pair (c1, c2) of the
+// head, reduced by out[(J,M), o] = sum_{c1,c2} wt[h][J][o][c1 m + c2] u[(J,M), c1, c2],
+// stored channel-pair packed into W (H*mo output channels, Cpo = H*mo/2
+// columns per component; rows as in CgArgs).
+struct InterArgs {
+  const float2* Z;  // forward spectra [B][N][K][C] (C = H*m)
+  float2* W;        // packed output spectra [B][N][K][Cpo]
+  const float* wt;  // [H][L+1][mo][m*m]
+  long long N;
+  int n1_log2, n2_log2;
+  int F;            // N/2 + 1
+  int B, C, H, m, mo, Cpo;
+};
+template <int L>
+hipError_t launch_cg_inter(const InterArgs& a, hipStream_t s);
+constexpr int kInterLmax = 6;
+constexpr int kInterMmax = 8;  // channels per head
+
 // Invariant softmax gating + real-space value tensor product (gate.hip), one
 // specialisation per L_max: u, v, f fp32 [B][N][K][C]; part holds
 // B * ceil(N / kGateChunk) * (L+1) * C online-softmax partials (maximum,
