@@ -38,13 +38,32 @@ __device__ __forceinline__ float swap_pair(float v) {
 // contraction keeps every lane active).  Written as volatile assembly so
 // that it stays where the generated code puts it, next to the products that
 // use it: as a builtin the compiler hoisted the partner values of a whole
-// phase and spilled them.
+// phase and spilled them.  A DPP move must follow the VALU write of its
+// source register by two wait states; the compiler inserts them for its own
+// DPP instructions but cannot see into inline assembly, so the s_nop is
+// part of the statement (the combine step reads an accumulator written by
+// the instruction just before).
 __device__ __forceinline__ float lane_partner(float v) {
   float r;
-  asm volatile("v_mov_b32_dpp %0, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1" : "=v"(r) : "v"(v));
+  asm volatile(
+      "s_nop 1\n\t"
+      "v_mov_b32_dpp %0, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+      : "=v"(r)
+      : "v"(v));
   return r;
 }
-__device__ __forceinline__ float2 lane_partner2(float2 v) { return make_float2(lane_partner(v.x), lane_partner(v.y)); }
+// both halves of a complex value, behind one s_nop (early-clobber outputs:
+// the first move must not overwrite the second one's source)
+__device__ __forceinline__ float2 lane_partner2(float2 v) {
+  float2 r;
+  asm volatile(
+      "s_nop 1\n\t"
+      "v_mov_b32_dpp %0, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+      "v_mov_b32_dpp %1, %3 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+      : "=&v"(r.x), "=&v"(r.y)
+      : "v"(v.x), "v"(v.y));
+  return r;
+}
 
 // value of the lane with index lane ^ 2 (quad_perm [2,3,0,1])
 __device__ __forceinline__ float swap_quad_pair(float v) {
