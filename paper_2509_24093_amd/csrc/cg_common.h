@@ -12,11 +12,11 @@ namespace cgdev {
 template <int L>
 struct CgBody;  // specialised by the generated cg_body_L<L>.inc files
 template <int L>
-struct CgPathBody;  // per-path variant for the channel-mixing kernel (same files)
-template <int L>
 struct CgRealBody;  // token-wise real-basis product of the value tensor product (same files)
 template <int L>
 struct CgSplitBody;  // lane-pair variant: one point per two lanes (same files)
+template <int L>
+struct CgPathSplitBody;  // lane-pair per-path variant for the channel-mixing kernel (same files)
 
 constexpr int kCgThreads = 256;
 
@@ -181,15 +181,16 @@ struct SplitPairStore {
 // their use (compiler memory barriers keep every group's loads together):
 // all K loads up front would need K registers more, and one group at a time
 // waited a full memory round trip per group.
-template <int K, class Arr>
+template <int K, int G = 16, class Arr>
 __device__ __forceinline__ void load_unpack_half(const CgArgs& a, const Point& pt, int half, Arr& x) {
   const bool cv = pt.valid && pt.c < a.C;
   const long long wn = (a.N - pt.w) & (a.N - 1);
   const int cl = pt.c < a.C ? pt.c : a.C - 1;
   const float2* z = a.Z + ((pt.b * a.N + freq_row(half ? wn : pt.w, a)) * K) * a.C + cl;
   // (groups of 8 with two or three in flight, or of 16 or 32 with one or
-  // two, measured the same or slower at L_max = 8)
-  constexpr int G = 16, D = 1, NG = (K + G - 1) / G;
+  // two, measured the same or slower at L_max = 8; G = 8 where the kernel
+  // has a third of the register file)
+  constexpr int D = 1, NG = (K + G - 1) / G;
   float2 buf[D + 1][G];
   auto issue = [&](int g) {
 #pragma unroll

@@ -6,14 +6,17 @@
 //
 // Built once per L_max (-DCGCONV_TU_L=<L>, -DCGCONV_BODY).  A block holds 8
 // frequency points (pairs w, N-w) x 32 channel slots (C <= 32) and has two
-// kinds of waves.  The four product waves (lane = point * 32 + channel)
-// evaluate the per-path products of their channel with the generated
-// CgPathBody (VALU), one step at a time (a step = the paths of one pair
-// (l1, l2) with degrees Ja..Jb, at most 24 outputs (J, M)); the values are
-// staged in LDS as a [c_in][column] matrix, column = (M, point, re/im), in
-// one of two buffers.  The four matrix-core waves run the dense mixing of
-// the previous step meanwhile: for every path of the step and every
-// 32-column tile of its output degree J,
+// kinds of waves.  The eight product waves hold one point per pair of lanes
+// (lane = (point * 32 + channel) * 2 + half; half 0 keeps qa, half 1
+// (-1)^l ka, as in the lane-pair contraction) and evaluate the per-path
+// products with the generated CgPathSplitBody (VALU), one step at a time: a
+// step is an unordered degree pair {l1, l2} with a run of output degrees,
+// the even lanes producing path (l1, l2, J) and the odd lanes path
+// (l2, l1, J) (for l1 == l2 the two lanes share one path).  The values are
+// staged in LDS as a [c_in][column] matrix, column = (slot, point, re/im),
+// the second path set after the first, in one of two buffers.  The four
+// matrix-core waves run the dense mixing of the previous step meanwhile:
+// for every path of the step and every 32-column tile of its output degree J,
 //   D[c_out][col] += sum_{c_in} W_p[c_out][c_in] * T[c_in][col]
 // in fp32 accumulation from bfloat16 operands split into two parts,
 // x = hi + lo (hi = bf16(x), lo = bf16(x - hi); |x - hi - lo| <= 2^-18 |x|):
@@ -28,10 +31,11 @@
 // packed, exactly like the unmixed stage.  Weights arrive split and
 // pre-arranged in the MFMA A-operand order (prepare_mix_weights) and are
 // copied a step ahead straight into the other of two LDS weight buffers
-// (global_load_lds); every MFMA operand is one 16-byte LDS read.  Keeping
-// the two kinds of work in different waves lets a SIMD issue the products
-// of one wave while the matrix core runs the other's MFMAs, and each kind
-// of wave needs only its own registers (inputs, or accumulators).
+// (global_load_lds); every MFMA operand is one 16-byte LDS read.  With K
+// instead of 2K input values per lane a product wave needs no more than a
+// third of a SIMD's registers, so every SIMD runs two product waves (which
+// hide each other's latencies and together issue at the two-wave rate) next
+// to the matrix-core wave.
 #include <hip/hip_runtime.h>
 
 #include "cg_common.h"
@@ -48,25 +52,26 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int kMixPts = 8;
 constexpr int kMixCh = 32;
-constexpr int kProducers = kMixPts * kMixCh;  // product lanes: 4 waves
-constexpr int kMixThreads = 2 * kProducers;   // + 4 matrix-core waves
+constexpr int kProducers = kMixPts * kMixCh * 2;  // product lanes: 8 waves, two lanes per point
 constexpr int kCWaves = 4;
+constexpr int kMixThreads = kProducers + 64 * kCWaves;  // + 4 matrix-core waves
 
 template <int L>
 struct MixGeo {
+  using Body = CgPathSplitBody<L>;
   static constexpr int K = (L + 1) * (L + 1);
   static constexpr int NT = (L + 1) * (L + 2) / 2;          // output tiles: J + 1 per degree J
   static constexpr int NTW = (NT + kCWaves - 1) / kCWaves;  // tiles per matrix-core wave
   static constexpr int NOUT = 32 * NT;                      // output columns (tile g at 32 g)
-  static constexpr int NIN = 16 * CgPathBody<L>::kMaxStepSlots + 16;  // staging of one step (+ overrun of a half tile)
+  static constexpr int NIN = 16 * Body::kMaxStepSlots + 16;  // staging of one step (+ overrun of a half tile)
   // A staged column is 32 channels of bfloat16 hi parts followed by 32 of lo
   // parts (128 B); rows of 36 words keep the 16-byte operand reads of 16
   // consecutive lanes (consecutive columns) on distinct banks.  Parked
   // output tiles use the same row stride with 32 fp32 channels.
   static constexpr int RS = 36;
-  static constexpr int T_WORDS = NIN * RS;                            // one staging buffer
-  static constexpr int W_WORDS = CgPathBody<L>::kMaxStepPaths * 1024;  // one weight buffer (4 KiB per path)
-  static constexpr int P_WORDS = NOUT * RS;                           // parked output tiles
+  static constexpr int T_WORDS = NIN * RS;                  // one staging buffer
+  static constexpr int W_WORDS = Body::kMaxStepPaths * 1024;  // one weight buffer (4 KiB per path)
+  static constexpr int P_WORDS = NOUT * RS;                 // parked output tiles
   static constexpr int WORDS = (2 * T_WORDS + 2 * W_WORDS) > P_WORDS ? (2 * T_WORDS + 2 * W_WORDS) : P_WORDS;
   static_assert(WORDS * 4 <= 160 * 1024, "LDS exceeds 160 KB");
 };
@@ -80,32 +85,40 @@ typedef float v2f __attribute__((ext_vector_type(2)));
 template <int L>
 struct MixProducer {
   using G = MixGeo<L>;
-  char* stage;  // LDS: two buffers of [col][RS words]: hi[32], lo[32] (bf16)
-  int c, pt;
+  char* sm;     // LDS base
+  int off;      // this lane's byte in column (slot 0, point, re) of buffer 0
+  int half;     // 0: even lane, 1: odd lane of the point
+  float hsign;  // -1 on the odd lane: its value of an odd degree J is -1 times the path value
 
   // value of slot s of the current step, columns 16 s + 2 pt (re) and + 1
-  // (im), split as v = hi + lo with hi = bf16(v), lo = bf16(v - hi)
-  template <int B>
-  __device__ __forceinline__ void put(int slot, float2 v) {
+  // (im), split as v = hi + lo with hi = bf16(v), lo = bf16(v - hi); the odd
+  // lane writes the second path set's slots (S0 on) when the step has one
+  template <int B, int S0>
+  __device__ __forceinline__ void put(int slot, float2 v, bool odd_J) {
+    if (odd_J) {
+      v.x *= hsign;
+      v.y *= hsign;
+    }
     const v2f x = {v.x, v.y};
     const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, v2bf));  // one packed conversion
     const v2f r = {v.x - __uint_as_float(h << 16), v.y - __uint_as_float(h & 0xffff0000u)};
     const uint32_t l = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, v2bf));
-    char* d = stage + B * (4 * G::T_WORDS) + (slot * 16 + pt * 2) * (4 * G::RS) + 2 * c;
+    char* d = sm + (off + half * (S0 * 16 * 4 * G::RS)) + (B * (4 * G::T_WORDS) + slot * 16 * (4 * G::RS));
     *reinterpret_cast<uint16_t*>(d) = (uint16_t)h;
     *reinterpret_cast<uint16_t*>(d + 64) = (uint16_t)l;
     *reinterpret_cast<uint16_t*>(d + 4 * G::RS) = (uint16_t)(h >> 16);
     *reinterpret_cast<uint16_t*>(d + 4 * G::RS + 64) = (uint16_t)(l >> 16);
   }
 
-  // the values of one M are staged: the compiler may not hoist the next M's
-  // products above them (that would keep more products live than registers
-  // hold next to the 196 input floats)
-  __device__ __forceinline__ void end_m() { __builtin_amdgcn_sched_barrier(0); }
-
   // the step's values are staged; the matrix-core waves take them after
   // this barrier while the product waves go on with the next step
-  __device__ __forceinline__ void end_step() { __syncthreads(); }
+  // (the lane's offsets become opaque at every step, so that the compiler
+  // computes the step's addresses in the step instead of keeping those of
+  // all steps alive)
+  __device__ __forceinline__ void end_step() {
+    __syncthreads();
+    asm volatile("" : "+v"(off), "+v"(half));
+  }
 };
 
 // Matrix-core waves: the dense mixing of each step, while the product waves
@@ -118,6 +131,7 @@ struct MixConsumer {
   char* wst;           // LDS: two weight buffers [path][step][hi/lo][64][8] (bf16)
   const uint16_t* wt;  // prepared split weights (global), same order per path
   int lane, cw;
+  int wl, sl;          // this lane's byte offsets in a weight buffer and a staging buffer
   v16f acc[G::NTW];
 
   // split weights of paths P0 .. P0+NP-1 into weight buffer dst (1 KB per
@@ -132,40 +146,54 @@ struct MixConsumer {
     }
   }
 
-  template <int P0, int NP>
+  // the weights of a step: the first path set, then the second (P0b < 0: none)
+  template <int P0a, int P0b, int NP>
+  __device__ __forceinline__ void copy_step_weights(char* dst) {
+    copy_weights<P0a, NP>(dst);
+    if constexpr (P0b >= 0) copy_weights<P0b, NP>(dst + NP * 4096);
+  }
+
+  template <int P0a, int P0b, int NP>
   __device__ __forceinline__ void first() {
-    copy_weights<P0, NP>(wst);
+    copy_step_weights<P0a, P0b, NP>(wst);
   }
 
   // the MFMA work of wave W for one step: every tile g of degree JA..JB with
-  // g mod 4 == W, as straight-line code
-  template <int W, int B, int JA, int JB>
-  __device__ __forceinline__ void tiles() {
-    int colJ = 0;  // first staging column of degree J within the step
+  // g mod 4 == W, for each of the step's path sets, as straight-line code
+  template <int W, int B, int JA, int JB, int S0, bool TWO>
+  __device__ __forceinline__ void tiles(int wl_, int sl_) {
+    constexpr int NP = JB - JA + 1;
 #pragma unroll
-    for (int J = JA; J <= JB; ++J) {
+    for (int h = 0; h < (TWO ? 2 : 1); ++h) {
+      int colJ = 16 * S0 * h;  // first staging column of degree J within the step
 #pragma unroll
-      for (int t = 0; t <= J; ++t) {
-        const int g = J * (J + 1) / 2 + t;  // global output tile
-        if (g % kCWaves == W) {             // compile-time
-          const char* wa = wst + B * (4 * G::W_WORDS) + (J - JA) * 4096 + lane * 16;
-          const char* tb =
-              stage + B * (4 * G::T_WORDS) + (colJ + 32 * t + (lane & 31)) * (4 * G::RS) + 16 * (lane >> 5);
-          v16f d = acc[g / kCWaves];
+      for (int J = JA; J <= JB; ++J) {
 #pragma unroll
-          for (int s = 0; s < 2; ++s) {  // input channels 16 s .. 16 s + 15
-            const v8bf ah = *reinterpret_cast<const v8bf*>(wa + s * 2048);
-            const v8bf al = *reinterpret_cast<const v8bf*>(wa + s * 2048 + 1024);
-            const v8bf bh = *reinterpret_cast<const v8bf*>(tb + 32 * s);
-            const v8bf bl = *reinterpret_cast<const v8bf*>(tb + 32 * s + 64);
-            d = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, d, 0, 0, 0);
-            d = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, d, 0, 0, 0);
-            d = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, d, 0, 0, 0);
+        for (int t = 0; t <= J; ++t) {
+          const int g = J * (J + 1) / 2 + t;  // global output tile
+          if (g % kCWaves == W) {             // compile-time
+            const char* wa = wst + wl_ + (B * (4 * G::W_WORDS) + (h * NP + J - JA) * 4096);
+            const char* tb = stage + sl_ + (B * (4 * G::T_WORDS) + (colJ + 32 * t) * (4 * G::RS));
+            v16f d = acc[g / kCWaves];
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {  // input channels 16 s .. 16 s + 15
+              const v8bf ah = *reinterpret_cast<const v8bf*>(wa + s * 2048);
+              const v8bf al = *reinterpret_cast<const v8bf*>(wa + s * 2048 + 1024);
+              const v8bf bh = *reinterpret_cast<const v8bf*>(tb + 32 * s);
+              const v8bf bl = *reinterpret_cast<const v8bf*>(tb + 32 * s + 64);
+              d = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, d, 0, 0, 0);
+              d = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, d, 0, 0, 0);
+              d = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, d, 0, 0, 0);
+            }
+            acc[g / kCWaves] = d;
+            // one tile's operands at a time: hoisting the next tiles' LDS
+            // reads would not fit next to the accumulators in a third of
+            // the register file
+            __builtin_amdgcn_sched_barrier(0);
           }
-          acc[g / kCWaves] = d;
         }
+        colJ += 16 * (2 * J + 1);
       }
-      colJ += 16 * (2 * J + 1);
     }
   }
 
@@ -173,26 +201,24 @@ struct MixConsumer {
   // wave's copies, then the barrier for every wave's), the product waves
   // have staged its values; the next step's weights go to the other buffer,
   // whose previous step every matrix-core wave finished before the barrier
-  template <int B, int P0, int JA, int JB, int P0N, int NPN>
+  template <int W, int B, int JA, int JB, int S0, bool TWO, int P0aN, int P0bN, int NPN>
   __device__ __forceinline__ void step() {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if constexpr (NPN > 0) copy_weights<P0N, NPN>(wst + (B ^ 1) * (4 * G::W_WORDS));
-    switch (cw) {  // uniform per wave
-      case 0: tiles<0, B, JA, JB>(); break;
-      case 1: tiles<1, B, JA, JB>(); break;
-      case 2: tiles<2, B, JA, JB>(); break;
-      default: tiles<3, B, JA, JB>(); break;
-    }
+    if constexpr (NPN > 0) copy_step_weights<P0aN, P0bN, NPN>(wst + (B ^ 1) * (4 * G::W_WORDS));
+    // opaque per step: the step's addresses are computed in the step
+    int wl_ = wl, sl_ = sl;
+    asm volatile("" : "+v"(wl_), "+v"(sl_));
+    tiles<W, B, JA, JB, S0, TWO>(wl_, sl_);
   }
 };
 
-// Waves 0-3 compute the per-path products of 8 points x 32 channels (lane =
-// point * 32 + channel); waves 4-7 run the mixing on the matrix cores one
-// step behind.  Both execute one barrier per step (the generated produce /
-// consume sequences have the same number of steps), then two more: after
-// the last step (the staging area becomes the parking area) and after the
-// mixed tiles are parked.
+// Waves 0-7 compute the per-path products of 8 points x 32 channels (lane =
+// (point * 32 + channel) * 2 + half); waves 8-11 run the mixing on the
+// matrix cores one step behind.  Both execute one barrier per step (the
+// generated produce / consume sequences have the same number of steps),
+// then two more: after the last step (the staging area becomes the parking
+// area) and after the mixed tiles are parked.
 template <int L>
 __global__ __launch_bounds__(kMixThreads, 1) void cg_mix_kernel(CgArgs a) {
   using G = MixGeo<L>;
@@ -201,30 +227,32 @@ __global__ __launch_bounds__(kMixThreads, 1) void cg_mix_kernel(CgArgs a) {
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: scalar branches
   if (wave < kProducers / 64) {
-    const long long gp = (long long)blockIdx.x * kMixPts + tid / kMixCh;
+    const int half = tid & 1, c = (tid >> 1) % kMixCh, ptl = tid / (2 * kMixCh);
+    const long long gp = (long long)blockIdx.x * kMixPts + ptl;
     const long long npts = a.npts / (2 * a.Cp);  // B * F points
     Point pt;
     pt.valid = gp < npts;
     const long long gpc = pt.valid ? gp : 0;
-    pt.c = tid % kMixCh;
+    pt.c = c;
     pt.w = gpc % a.F;
     pt.b = gpc / a.F;
-    float2 qa[K], ka[K];
-    load_unpack<K>(a, pt, qa, ka);
+    float2 x[K];
+    load_unpack_half<K, 8>(a, pt, half, x);  // groups of 8: a third of the register file
     MixProducer<L> st;
-    st.stage = reinterpret_cast<char*>(smem);
-    st.c = pt.c;
-    st.pt = tid / kMixCh;
-    CgPathBody<L>::produce(qa, ka, st);
+    st.sm = reinterpret_cast<char*>(smem);
+    st.off = (ptl * 2) * (4 * G::RS) + 2 * c;
+    st.half = half;
+    st.hsign = half ? -1.f : 1.f;
+    CgPathSplitBody<L>::produce(x, st);
     __syncthreads();  // the matrix-core waves finish the last step
     __syncthreads();  // the mixed tiles are parked
-    // this lane's mixed complex-basis values w[J, M] (columns 32 J(J+1)/2 +
+    // this point's mixed complex-basis values w[J, M] (columns 32 J(J+1)/2 +
     // 16 (M+J) + 2 pt + {0, 1}), converted to the real basis and stored
-    // channel-pair packed as in the unmixed stage
+    // channel-pair packed as in the unmixed stage (half 0 writes)
     Point ps = pt;
     ps.valid = pt.valid && pt.c < 2 * a.Cp;
-    PairStore out = make_store(a, ps, K);
-    const float* base = smem + (2 * st.pt) * G::RS + pt.c;
+    SplitPairStore out = make_split_store(a, ps, half, K);
+    const float* base = smem + (2 * ptl) * G::RS + c;
     auto w_at = [&](int J, int M) {
       const float* e = base + (32 * (J * (J + 1) / 2) + 16 * (M + J)) * G::RS;
       return make_float2(e[0], e[G::RS]);
@@ -246,9 +274,16 @@ __global__ __launch_bounds__(kMixThreads, 1) void cg_mix_kernel(CgArgs a) {
     st.wt = a.wmix;
     st.lane = tid & 63;
     st.cw = wave - kProducers / 64;
+    st.wl = st.lane * 16;
+    st.sl = (st.lane & 31) * (4 * G::RS) + 16 * (st.lane >> 5);
 #pragma unroll
     for (int i = 0; i < G::NTW; ++i) st.acc[i] = v16f{};
-    CgPathBody<L>::consume(st);
+    switch (st.cw) {  // uniform per wave: one straight-line sequence per matrix-core wave
+      case 0: CgPathSplitBody<L>::template consume<0>(st); break;
+      case 1: CgPathSplitBody<L>::template consume<1>(st); break;
+      case 2: CgPathSplitBody<L>::template consume<2>(st); break;
+      default: CgPathSplitBody<L>::template consume<3>(st); break;
+    }
     __syncthreads();  // every step's MFMAs are done: the staging area is free
     // park the mixed tiles: D row i = c_out, column 32 g + (lane & 31),
     // stored as [column][RS] with the channels in natural order

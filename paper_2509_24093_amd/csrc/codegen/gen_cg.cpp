@@ -32,9 +32,11 @@
 // cg_common.h): written as ordinary C++, the compiler turns -(a*b) into
 // a*(-b) and keeps a negated copy of every input alive for the whole kernel.
 //
-// A second body per L, CgPathBody<L>, keeps the paths apart for the
-// channel-mixing kernel, in steps (see emit_path_body); a third, CgRealBody<L>, is the
-// token-wise real-basis product of the value tensor product (emit_real_body).
+// Further bodies per L: CgSplitBody<L>, the lane-pair form of the same
+// contraction (emit_split_body); CgPathSplitBody<L>, which keeps the paths
+// apart for the channel-mixing kernel, in steps (emit_path_split_body); and
+// CgRealBody<L>, the token-wise real-basis product of the value tensor
+// product (emit_real_body).
 //
 // Usage: gen_cg <output-dir> <LGEN>   (writes cg_body_L<L>.inc and cg_lgen.h)
 #include <algorithm>
@@ -324,134 +326,187 @@ void emit_body(FILE* f, int L, long* ops_out) {
 
 }  // namespace
 
-// Per-path body for the channel-mixing kernel: the products of every path
-// p = (l1, l2, J) are kept apart, and the work is cut into steps small enough
-// to double-buffer their staged values in LDS.  Pairs (l1, l2) are taken in
-// lexicographic order (path indices follow the (l1, l2, J) order of the
-// weights); a pair's degrees J are cut, from the top, into runs Ja..Jb of at
-// most kStepSlotBudget outputs (J, M).  A step evaluates, M by M, the
-// products qa[l1,m1] * ka[l2,M-m1] (4 ops, shared by the J of the step) and
-// the values w_p[M] of its paths, each handed to st.put<B>(slot, value)
-// with B = step parity and slot = the position of (J, M) among the step's
-// outputs (J ascending, then M = -J..J), zeros included; st.end_m() follows
-// each M and st.end_step() each step.  CgPathBody<L>::produce is that sequence;
-// CgPathBody<L>::consume is the matching sequence of
-// st.step<B, P0, Ja, Jb, P0n, NPn>() calls (the step's first path and degree
-// range, and the first path and path count of the next step, NPn = 0 after
-// the last), preceded by st.first<P0, NP>() for the first step's weights.
-// A step that splits a pair recomputes the products its degrees need.
-constexpr int kStepSlotBudget = 24;
+// Lane-pair per-path body for the channel-mixing kernel
+// (CgPathSplitBody<L>): one point per pair of adjacent lanes as in
+// CgSplitBody (even lane x = qa, odd lane x[(l,m)] = (-1)^l ka[(l,m)]), the
+// products of every path kept apart.  The work is cut into pair steps over
+// unordered degree pairs {l1 <= l2}, each with a run Ja..Jb of output
+// degrees (at most kPairHalfSlots outputs (J, M) and kPairHalfPaths degrees).
+// In a step with l1 < l2 every product x[(l1,m1)] * partner(x[(l2,m2)]),
+// taken with the coefficient (-1)^l2 c((l1,m1),(l2,m2),J), is a term of path
+// (l1, l2, J) in the even lane and (-1)^J times a term of path (l2, l1, J)
+// in the odd lane (swap symmetry c(q,o,J) = (-1)^(l1+l2-J) c(o,q,J), checked
+// for every pair): the two lanes evaluate the two ordered paths at once.  In
+// a step with l1 == l2 both ordered terms of an unordered pair belong to the
+// same path: as in CgSplitBody the lanes take one each (diagonal pairs half
+// the coefficient) and combine, w = acc + (-1)^J partner(acc).  Either way
+// the odd lane's value is (-1)^J times its path value; st.put<B, S0>(slot,
+// value, odd_J) corrects the sign and stages the value at slot (odd lanes
+// at slot + S0, the second path's slots, when l1 < l2; the same slot as the
+// even lane, with the same value, when l1 == l2).  Slots follow J ascending,
+// then M = -J..J, zeros included; st.end_step() follows each step.
+// CgPathSplitBody<L>::consume<W> is, for matrix-core wave W, the matching
+// sequence of st.step<W, B, JA, JB, S0, TWO, P0aN, P0bN, NPN>() calls (TWO: the step has
+// the second path set; P0aN, P0bN, NPN: the first paths of the next step's
+// two path sets and their length, NPN = 0 after the last step), preceded by
+// st.first<P0a, P0b, NP>() (P0b = -1 without a second set).
+constexpr int kPairHalfSlots = 13;
+constexpr int kPairHalfPaths = 2;
 
-struct MixStep {
-  int l1, l2, Ja, Jb, P0;
+struct PairStep {
+  int l1, l2, Ja, Jb, P0a, P0b;  // P0b = -1 when l1 == l2
 };
 
-std::vector<MixStep> mix_steps(int L) {
-  std::vector<MixStep> steps;
+int path_index(int L, int l1, int l2, int J) {
   int path = 0;
-  for (int l1 = 0; l1 <= L; ++l1)
-    for (int l2 = 0; l2 <= L; ++l2) {
-      const int Jmin = std::abs(l1 - l2), Jmax = std::min(l1 + l2, L);
+  for (int a = 0; a <= L; ++a)
+    for (int b = 0; b <= L; ++b) {
+      const int Jmin = std::abs(a - b), Jmax = std::min(a + b, L);
       if (Jmin > Jmax) continue;
+      if (a == l1 && b == l2) return path + (J - Jmin);
+      path += Jmax - Jmin + 1;
+    }
+  std::fprintf(stderr, "gen_cg: no path (%d %d %d)\n", l1, l2, J);
+  std::exit(1);
+}
+
+std::vector<PairStep> pair_steps(int L) {
+  std::vector<PairStep> steps;
+  for (int l1 = 0; l1 <= L; ++l1)
+    for (int l2 = l1; l2 <= L; ++l2) {
+      const int Jmin = l2 - l1, Jmax = std::min(l1 + l2, L);
+      if (Jmin > Jmax) continue;
+      // a step with l1 == l2 stages one path set and may take both halves' room
+      const int slot_cap = l1 == l2 ? 2 * kPairHalfSlots : kPairHalfSlots;
+      const int path_cap = l1 == l2 ? 2 * kPairHalfPaths : kPairHalfPaths;
       int J = Jmax;
       while (J >= Jmin) {
         const int Jb = J;
-        int slots = 2 * J + 1;
+        int slots = 2 * J + 1, n = 1;
         --J;
-        while (J >= Jmin && slots + 2 * J + 1 <= kStepSlotBudget) slots += 2 * J-- + 1;
-        steps.push_back({l1, l2, J + 1, Jb, path + (J + 1 - Jmin)});
+        while (J >= Jmin && n < path_cap && slots + 2 * J + 1 <= slot_cap) {
+          slots += 2 * J-- + 1;
+          ++n;
+        }
+        const int Ja = J + 1;
+        steps.push_back({l1, l2, Ja, Jb, path_index(L, l1, l2, Ja), l1 == l2 ? -1 : path_index(L, l2, l1, Ja)});
       }
-      path += Jmax - Jmin + 1;
     }
   return steps;
 }
 
-void emit_path_body(FILE* f, int L, long* ops_out) {
+void emit_path_split_body(FILE* f, int L, long* ops_out) {
   const int K = (L + 1) * (L + 1);
   std::vector<Term> terms = contraction_terms(L);
-  std::map<std::array<int, 3>, std::vector<Term>> by_pair_M;  // (l1, l2, M) -> terms
-  for (const Term& t : terms) by_pair_M[{t.l1, t.l2, t.M}].push_back(t);
-  const std::vector<MixStep> steps = mix_steps(L);
-  long ops = 0;
-  int max_slots = 0, max_paths = 0, n_paths = 0;
-  for (const MixStep& st : steps) n_paths = std::max(n_paths, st.P0 + st.Jb - st.Ja + 1);
-  std::fprintf(f, "template <>\nstruct CgPathBody<%d> {\n  static constexpr int K = %d;\n", L, K);
+  TermMap terms_of;
+  for (const Term& t : terms) terms_of[{t.l1, t.m1, t.l2, t.m2}].push_back(t);
+  const std::vector<PairStep> steps = pair_steps(L);
+  Emitter e{f, {}, 0};
+  int max_slots = 0, max_paths = 0;
+  auto sname = [](int J, int M) { return "s" + std::to_string(J) + "_" + std::to_string(M + J); };
+  std::fprintf(f, "template <>\nstruct CgPathSplitBody<%d> {\n  static constexpr int K = %d;\n", L, K);
   std::fprintf(f, "  template <class Store>\n");
-  std::fprintf(f,
-               "  static __device__ __forceinline__ void produce(const float2 (&qa)[%d], const float2 (&ka)[%d], "
-               "Store& st) {\n",
-               K, K);
+  std::fprintf(f, "  static __device__ __forceinline__ void produce(const float2 (&x)[%d], Store& st) {\n", K);
   for (size_t si = 0; si < steps.size(); ++si) {
-    const MixStep& sp = steps[si];
+    const PairStep& sp = steps[si];
     const int B = (int)(si & 1);
-    int slots = 0;
-    for (int J = sp.Ja; J <= sp.Jb; ++J) slots += 2 * J + 1;
-    max_slots = std::max(max_slots, slots);
-    max_paths = std::max(max_paths, sp.Jb - sp.Ja + 1);
-    std::fprintf(f, "    {  // step %zu: pair l1=%d l2=%d, J = %d..%d (paths %d..%d)\n", si, sp.l1, sp.l2, sp.Ja, sp.Jb,
-                 sp.P0, sp.P0 + sp.Jb - sp.Ja);
-    for (int M = -sp.Jb; M <= sp.Jb; ++M) {
-      auto it = by_pair_M.find({sp.l1, sp.l2, M});
-      std::map<int, std::vector<const Term*>> by_m1;
-      if (it != by_pair_M.end())
-        for (const Term& t : it->second)
-          if (t.J >= sp.Ja && t.J <= sp.Jb) by_m1[t.m1].push_back(&t);
-      std::fprintf(f, "    {  // M = %d\n", M);
-      std::set<int> inited;
-      for (int J = std::max(sp.Ja, std::abs(M)); J <= sp.Jb; ++J) std::fprintf(f, "      float2 t%d;\n", J);
-      for (auto& e : by_m1) {
-        const int m1 = e.first, m2 = M - m1;
-        const std::string q = qname(sp.l1, m1), k = kname(sp.l2, m2);
-        std::fprintf(f, "      { const float pr = fnma(%s.y, %s.y, %s.x * %s.x);", q.c_str(), k.c_str(), q.c_str(),
-                     k.c_str());
-        std::fprintf(f, " const float pi = fmaf(%s.y, %s.x, %s.x * %s.y);\n", q.c_str(), k.c_str(), q.c_str(),
-                     k.c_str());
-        ops += 4;
-        for (const Term* t : e.second) {
-          const std::string a = "t" + std::to_string(t->J);
-          const std::string re_src = t->imag ? "pi" : "pr", im_src = t->imag ? "pr" : "pi";
-          const double re_c = t->imag ? -t->coef : t->coef, im_c = t->coef;
-          if (!inited.count(t->J))
-            std::fprintf(f, "      %s.x = %s * %s; %s.y = %s * %s;\n", a.c_str(), lit(re_c).c_str(),
-                         re_src.c_str(), a.c_str(), lit(im_c).c_str(), im_src.c_str());
-          else
-            std::fprintf(f, "      %s.x = fmaf(%s, %s, %s.x); %s.y = fmaf(%s, %s, %s.y);\n", a.c_str(),
-                         lit(re_c).c_str(), re_src.c_str(), a.c_str(), a.c_str(), lit(im_c).c_str(),
-                         im_src.c_str(), a.c_str());
-          inited.insert(t->J);
-          ops += 2;
+    const bool two = sp.l1 != sp.l2;
+    int S0 = 0;
+    for (int J = sp.Ja; J <= sp.Jb; ++J) S0 += 2 * J + 1;
+    max_slots = std::max(max_slots, two ? 2 * S0 : S0);
+    max_paths = std::max(max_paths, (two ? 2 : 1) * (sp.Jb - sp.Ja + 1));
+    std::fprintf(f, "    {  // step %zu: degrees %d, %d, J = %d..%d\n", si, sp.l1, sp.l2, sp.Ja, sp.Jb);
+    for (int J = sp.Ja; J <= sp.Jb; ++J)
+      for (int M = -J; M <= J; ++M) std::fprintf(f, "      float2 %s;\n", sname(J, M).c_str());
+    for (int m2 = -sp.l2; m2 <= sp.l2; ++m2) {
+      const int q = comp(sp.l2, m2);
+      std::vector<std::pair<int, const std::vector<Term>*>> prods;  // (m1, terms)
+      for (int m1 = -sp.l1; m1 <= sp.l1; ++m1) {
+        if (!two && m1 > m2) continue;  // unordered pairs o <= q
+        auto it = terms_of.find({sp.l1, m1, sp.l2, m2});
+        if (it == terms_of.end()) continue;
+        bool any = false;
+        for (const Term& t : it->second) any |= t.J >= sp.Ja && t.J <= sp.Jb;
+        if (!any) continue;
+        // swap symmetry of the pair, which both lane roles rely on
+        auto sw = terms_of.find({sp.l2, m2, sp.l1, m1});
+        if (sw == terms_of.end() || sw->second.size() != it->second.size()) {
+          std::fprintf(stderr, "gen_cg: swap partner missing (per-path split body)\n");
+          std::exit(1);
         }
+        for (const Term& t : it->second) {
+          const Term* u = nullptr;
+          for (const Term& w : sw->second)
+            if (w.J == t.J) u = &w;
+          const double sigma = ((t.l1 + t.l2 - t.J) % 2 == 0) ? 1.0 : -1.0;
+          if (!u || u->imag != t.imag || std::fabs(u->coef - sigma * t.coef) > 1e-12 * std::fabs(t.coef) + 1e-15) {
+            std::fprintf(stderr, "gen_cg: swap symmetry violated (per-path split body)\n");
+            std::exit(1);
+          }
+          if (!two && m1 == m2 && t.J % 2 != 0) {
+            std::fprintf(stderr, "gen_cg: diagonal term of odd J (per-path split body)\n");
+            std::exit(1);
+          }
+        }
+        prods.push_back({m1, &it->second});
+      }
+      if (prods.empty()) continue;
+      std::fprintf(f, "      { const float2 pq = lane_partner2(x[%d]);\n", q);
+      e.ops += 2;
+      for (auto& pr : prods) {
+        const int m1 = pr.first, o = comp(sp.l1, m1);
+        std::fprintf(f, "      { const float pr = fnma(x[%d].y, pq.y, x[%d].x * pq.x);", o, o);
+        std::fprintf(f, " const float pi = fmaf(x[%d].y, pq.x, x[%d].x * pq.y);\n", o, o);
+        e.ops += 4;
+        const double scale = ((sp.l2 % 2) ? -1.0 : 1.0) * (!two && m1 == m2 ? 0.5 : 1.0);
+        for (const Term& t : *pr.second)
+          if (t.J >= sp.Ja && t.J <= sp.Jb) e.acc_add_scaled(sname(t.J, t.M), scale * t.coef, t.imag, "pr", "pi");
         std::fprintf(f, "      }\n");
       }
-      int base = 0;
-      for (int J = sp.Ja; J <= sp.Jb; ++J) {
-        if (std::abs(M) <= J) {
-          if (!inited.count(J)) std::fprintf(f, "      t%d = make_float2(0.f, 0.f);\n", J);
-          std::fprintf(f, "      st.template put<%d>(%d, t%d);\n", B, base + M + J, J);
-        }
-        base += 2 * J + 1;
-      }
-      std::fprintf(f, "      st.end_m();\n    }\n");
+      std::fprintf(f, "      }\n");
+      std::fprintf(f, "      __builtin_amdgcn_sched_barrier(0);\n");
     }
+    int base = 0;
+    for (int J = sp.Ja; J <= sp.Jb; ++J) {
+      for (int M = -J; M <= J; ++M) {
+        const std::string a = sname(J, M);
+        if (!e.inited.count(a)) {
+          std::fprintf(f, "      %s = make_float2(0.f, 0.f);\n", a.c_str());
+        } else if (!two) {
+          const char* op = J % 2 ? "-" : "+";
+          std::fprintf(f, "      %s.x = %s.x %s lane_partner(%s.x); %s.y = %s.y %s lane_partner(%s.y);\n", a.c_str(),
+                       a.c_str(), op, a.c_str(), a.c_str(), a.c_str(), op, a.c_str());
+          e.ops += 4;
+        }
+        std::fprintf(f, "      st.template put<%d, %d>(%d, %s, %s);\n", B, two ? S0 : 0, base + M + J, a.c_str(),
+                     J % 2 ? "true" : "false");
+      }
+      base += 2 * J + 1;
+    }
+    e.inited.clear();
     std::fprintf(f, "      st.end_step();\n    }\n");
   }
   std::fprintf(f, "  }\n");
-  std::fprintf(f, "  template <class Store>\n  static __device__ __forceinline__ void consume(Store& st) {\n");
-  std::fprintf(f, "    st.template first<%d, %d>();\n", steps[0].P0, steps[0].Jb - steps[0].Ja + 1);
+  std::fprintf(f, "  template <int W, class Store>\n  static __device__ __forceinline__ void consume(Store& st) {\n");
+  std::fprintf(f, "    st.template first<%d, %d, %d>();\n", steps[0].P0a, steps[0].P0b, steps[0].Jb - steps[0].Ja + 1);
   for (size_t si = 0; si < steps.size(); ++si) {
-    const MixStep& sp = steps[si];
-    const int P0n = si + 1 < steps.size() ? steps[si + 1].P0 : 0;
-    const int NPn = si + 1 < steps.size() ? steps[si + 1].Jb - steps[si + 1].Ja + 1 : 0;
-    std::fprintf(f, "    st.template step<%d, %d, %d, %d, %d, %d>();\n", (int)(si & 1), sp.P0, sp.Ja, sp.Jb, P0n,
-                 NPn);
+    const PairStep& sp = steps[si];
+    int S0 = 0;
+    for (int J = sp.Ja; J <= sp.Jb; ++J) S0 += 2 * J + 1;
+    const bool last = si + 1 == steps.size();
+    const PairStep* nx = last ? nullptr : &steps[si + 1];
+    std::fprintf(f, "    st.template step<W, %d, %d, %d, %d, %s, %d, %d, %d>();\n", (int)(si & 1), sp.Ja, sp.Jb, S0,
+                 sp.l1 != sp.l2 ? "true" : "false", nx ? nx->P0a : 0, nx ? nx->P0b : -1,
+                 nx ? nx->Jb - nx->Ja + 1 : 0);
   }
   std::fprintf(f, "  }\n");
-  std::fprintf(f, "  static constexpr int kPaths = %d;\n", n_paths);
   std::fprintf(f, "  static constexpr int kSteps = %d;\n", (int)steps.size());
-  std::fprintf(f, "  static constexpr int kMaxStepSlots = %d;  // most outputs (J, M) of one step\n", max_slots);
+  std::fprintf(f, "  static constexpr int kMaxStepSlots = %d;  // most staged outputs of one step (both paths)\n",
+               max_slots);
   std::fprintf(f, "  static constexpr int kMaxStepPaths = %d;  // most paths of one step\n", max_paths);
-  std::fprintf(f, "  static constexpr long kOps = %ld;  // VALU ops of the per-path products per point\n};\n\n", ops);
-  *ops_out = ops;
+  std::fprintf(f, "  static constexpr long kOps = %ld;  // VALU ops of the products per lane (two lanes per point)\n};\n\n",
+               e.ops);
+  *ops_out = e.ops;
 }
 
 // Lane-pair body for L_max 7 and 8 (CgSplitBody<L>::run(x, st)): one point
@@ -661,15 +716,16 @@ int main(int argc, char** argv) {
     }
     std::fprintf(f, "// Generated by csrc/codegen/gen_cg.cpp -- do not edit.\n");
     std::fprintf(f, "// Frequency-domain CG contraction body, L_max = %d.\n#pragma once\n\n", L);
-    long ops = 0, pops = 0, rops = 0, sops = 0;
+    long ops = 0, rops = 0, sops = 0, psops = 0;
     emit_body(f, L, &ops);
-    emit_path_body(f, L, &pops);
     emit_real_body(f, L, &rops);
     emit_split_body(f, L, &sops);
+    emit_path_split_body(f, L, &psops);
     std::fclose(f);
     std::fprintf(stderr,
-                 "gen_cg: L=%d ops/point=%ld per-path ops/point=%ld real token-wise ops=%ld lane-pair ops/lane=%ld\n",
-                 L, ops, pops, rops, sops);
+                 "gen_cg: L=%d ops/point=%ld real token-wise ops=%ld lane-pair ops/lane=%ld "
+                 "per-path lane-pair ops/lane=%ld\n",
+                 L, ops, rops, sops, psops);
   }
   const std::string hpath = dir + "/cg_lgen.h";
   FILE* h = std::fopen(hpath.c_str(), "w");

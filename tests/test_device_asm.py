@@ -101,8 +101,9 @@ def gen_dir(tmp_path_factory):
 
 
 # kernels with DPP moves: the lane-pair contraction (L_max 7; 8 is the same
-# code), the fused kernel's channel-pair stores and the inter-channel kernel
-UNITS = [("cg_gen.hip", 7), ("cg_fused.hip", 6), ("cg_inter.hip", 4)]
+# code), the fused kernel's channel-pair stores, the inter-channel kernel and the
+# lane-pair channel-mixing kernel
+UNITS = [("cg_gen.hip", 7), ("cg_fused.hip", 6), ("cg_inter.hip", 4), ("cg_mix.hip", 3)]
 
 
 @pytest.mark.parametrize("unit", UNITS, ids=lambda u: "%s-L%d" % u)
