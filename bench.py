@@ -275,6 +275,9 @@ def dft_length(N, boundary):
     return n
 
 
+KERNEL_OF_STAGE = {"cg_fused": "cg_fused_kernel", "cg_small": "cg_small_kernel"}
+
+
 def cg_roofline(stage_avg, B, N, L, C, n_products, nnz, traffic, traffic_src):
     """Roofline object of the CG stage (fused or unfused) from its average
     launch time: algorithmic flops per launch against the fp32 vector peak."""
@@ -283,7 +286,7 @@ def cg_roofline(stage_avg, B, N, L, C, n_products, nnz, traffic, traffic_src):
     F = N // 2 + 1
     points = B * F * C
     cg_flops_per_point = 6 * n_products + 4 * nnz
-    dom = "cg_fused" if "cg_fused" in stage_avg else "cg"
+    dom = "cg_fused" if "cg_fused" in stage_avg else ("cg_small" if "cg_small" in stage_avg else "cg")
     cg_ms = stage_avg[dom]
     flops = points * cg_flops_per_point
     flop_model = (f"(6*{n_products} distinct complex products + 4*{nnz} non-zeros) per "
@@ -296,9 +299,15 @@ def cg_roofline(stage_avg, B, N, L, C, n_products, nnz, traffic, traffic_src):
         dft = 5 * 64 * 6
         flops += dft * B * n1 * K * (C + Cp)
         flop_model += f" + {dft}-flop length-64 DFTs on {B * n1 * K * (C + Cp)} columns"
+    elif dom == "cg_small":
+        # the one-block kernel runs both whole DFTs: 5 N log2 N flops per
+        # complex transform, K*C forward and K*ceil(C/2) inverse columns
+        dft = 5 * N * (N.bit_length() - 1)
+        flops += dft * B * K * (C + Cp)
+        flop_model += f" + {dft}-flop length-{N} DFTs on {B * K * (C + Cp)} columns"
     achieved_tflops = flops / (cg_ms * 1e-3) / 1e12
     return {
-        "kernel": f"{'cg_fused_kernel' if dom == 'cg_fused' else ('cg_split_kernel' if L >= 7 else 'cg_gen_kernel')}<{L}>",
+        "kernel": f"{KERNEL_OF_STAGE.get(dom) or ('cg_split_kernel' if L >= 7 else 'cg_gen_kernel')}<{L}>",
         "bound": "alu",
         "achieved": round(achieved_tflops, 2),
         "peak": round(VALU_PEAK_TFLOPS, 1),
@@ -400,6 +409,8 @@ def main():
     Sp = B * Nf * K * Cp * 8
     if "cg_fused" in stage_avg:
         io = {"fft_fwd_1": 2 * S + 2 * Sc, "cg_fused": 2 * Sc + Sp, "fft_inv_2": Sp + S}
+    elif "cg_small" in stage_avg:
+        io = {"cg_small": 3 * S}
     elif Nf > 256:
         io = {"fft_fwd_1": 2 * S + 2 * Sc, "fft_fwd_2": 4 * Sc, "cg": 2 * Sc + Sp, "fft_inv_1": 2 * Sp,
               "fft_inv_2": Sp + S}

@@ -78,6 +78,8 @@ enum cgconv_status {
  * the same accuracy; they exist for cross-checks and tests):
  *   CGCONV_UNFUSED=1        the modular five-kernel pipeline instead of the
  *                           fused middle kernel;
+ *   CGCONV_NO_SMALL=1       for DFT lengths <= 256, the three single-pass
+ *                           kernels instead of the one-block kernel;
  *   CGCONV_FORCE_GENERIC=1  the table-driven contraction kernel instead of the
  *                           generated per-L_max bodies (modular pipeline);
  *   CGCONV_TEST_FAIL_ALLOC=1  token plans return NULL with the message of a

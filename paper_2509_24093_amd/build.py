@@ -24,6 +24,7 @@ LGEN = 8  # highest L_max with a generated register-resident contraction
 FUSED_LMAX = 6  # highest L_max with a fused (second pass + CG + inverse first pass) kernel
 MIX_LMAX = 6  # highest L_max with a channel-mixing (MFMA) CG stage
 INTER_LMAX = 6  # highest L_max with an inter-channel (MFMA reduction) CG stage
+SMALL_LMAX = 6  # highest L_max with the one-block kernel for DFT lengths <= 256
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed FP32 instructions are disabled for all device code.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -71,6 +72,9 @@ def build(jobs: int | None = None, verbose: bool = True) -> str:
                       ["-DCGCONV_TU_L=%d" % L, '-DCGCONV_BODY="cg_body_L%d.inc"' % L]))
     for L in range(INTER_LMAX, -1, -1):
         units.append(([HIPCC, "-c"] + HIP_FLAGS, "cg_inter.hip", "cg_inter_L%d.o" % L,
+                      ["-DCGCONV_TU_L=%d" % L, '-DCGCONV_BODY="cg_body_L%d.inc"' % L]))
+    for L in range(SMALL_LMAX, -1, -1):
+        units.append(([HIPCC, "-c"] + HIP_FLAGS, "cg_small.hip", "cg_small_L%d.o" % L,
                       ["-DCGCONV_TU_L=%d" % L, '-DCGCONV_BODY="cg_body_L%d.inc"' % L]))
     for L in range(LGEN, -1, -1):
         units.append(([HIPCC, "-c"] + HIP_FLAGS, "gate.hip", "gate_L%d.o" % L,

@@ -73,6 +73,8 @@ struct cgconv_plan {
   int L = 0, K = 0;
   int64_t N1 = 0, N2 = 0;  // N1 == 0: single pass
   bool fused = false;      // two-pass with N2 = 64 and the fused middle kernel
+  bool small = false;      // DFT length <= 256: the forward is one block per channel group (cg_small.hip)
+  int small_cc = 0, small_threads = 0;
   int device = 0;
   int64_t nnz = 0, paths = 0, products = 0;  // nnz: complex-basis terms the contraction evaluates
   // the real-basis tensor the plan's kernels evaluate (cgconv_plan_export_table)
@@ -126,6 +128,7 @@ void free_plan(cgconv_plan* p) {
 const char* const kStages2[] = {"fft_fwd_1", "fft_fwd_2", "cg", "fft_inv_1", "fft_inv_2"};
 const char* const kStages1[] = {"fft_fwd", "cg", "fft_inv"};
 const char* const kStagesF[] = {"fft_fwd_1", "cg_fused", "fft_inv_2"};
+const char* const kStagesS[] = {"cg_small"};
 const char* const kStagesM2[] = {"fft_fwd_1", "fft_fwd_2", "cg_mix", "fft_inv_1", "fft_inv_2"};
 const char* const kStagesM1[] = {"fft_fwd", "cg_mix", "fft_inv"};
 const char* const kStagesG[] = {"gate_partials", "gate_finalize", "gate_value"};
@@ -140,6 +143,7 @@ constexpr int kKindGate = 3;
 constexpr int kKindGateBwd = 5;
 constexpr int kKindGraph = 4;
 constexpr int kKindInter = 6;
+constexpr int kKindSmall = 7;
 constexpr int kMaxEvents = 8;  // stages + 1 of the longest pipeline
 
 hipError_t launch_product(int L, const GftProductArgs& a, hipStream_t s) {
@@ -212,6 +216,35 @@ hipError_t launch_inter(int L, const InterArgs& a, hipStream_t s) {
     default: return hipErrorInvalidValue;
   }
 }
+
+hipError_t launch_small(int L, const SmallArgs& a, hipStream_t s) {
+  switch (L) {
+    case 0: return launch_cg_small<0>(a, s);
+    case 1: return launch_cg_small<1>(a, s);
+    case 2: return launch_cg_small<2>(a, s);
+    case 3: return launch_cg_small<3>(a, s);
+    case 4: return launch_cg_small<4>(a, s);
+    case 5: return launch_cg_small<5>(a, s);
+    case 6: return launch_cg_small<6>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t prepare_small(int L, int lds_bytes) {
+  switch (L) {
+    case 0: return prepare_cg_small<0>(lds_bytes);
+    case 1: return prepare_cg_small<1>(lds_bytes);
+    case 2: return prepare_cg_small<2>(lds_bytes);
+    case 3: return prepare_cg_small<3>(lds_bytes);
+    case 4: return prepare_cg_small<4>(lds_bytes);
+    case 5: return prepare_cg_small<5>(lds_bytes);
+    case 6: return prepare_cg_small<6>(lds_bytes);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// LDS bytes of the one-block kernel for cc channels per block
+int64_t small_lds_bytes(int64_t Nf, int K, int cc) { return (Nf * K * cc + Nf) * 8; }
 
 hipError_t launch_fused(int L, const FusedArgs& a, hipStream_t s) {
   switch (L) {
@@ -310,7 +343,8 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
   const long long Nu = p->Nu;  // rows of q, k and out (padded rows are implicit zeros)
   const float inv_n = 1.0f / (float)N;
   hipEvent_t* ev = nullptr;  // events of this call if it is timed
-  const int kind = mix ? 1 : (scales ? 2 : 0);  // 2: one half of a backward
+  const bool small = p->small && !mix && !scales;
+  const int kind = mix ? 1 : (scales ? 2 : (small ? kKindSmall : 0));  // 2: one half of a backward
   if (p->timing_calls < p->timing_max && (p->timing_kind < 0 || p->timing_kind == kind)) {
     p->timing_kind = kind;
     ev = &p->events[(size_t)p->timing_calls * kMaxEvents];
@@ -326,7 +360,31 @@ int run_forward(cgconv_plan* p, const void* q, const void* k, void* out, bool bf
     e = launch_prepare_mix_weights(weights, p->d_wmix, (int)p->paths, (int)p->C, s);
     if (e != hipSuccess) goto fail;
   }
-  if (p->fused && !mix) {
+  if (small) {
+    // the whole convolution in one kernel: load, DFT, contraction, inverse
+    // DFT and store per (batch element, channel group), spectra in LDS
+    SmallArgs sa;
+    sa.q = q;
+    sa.k = k;
+    sa.out = out;
+    sa.tw = p->tw;
+    sa.B = (int)p->B;
+    sa.C = (int)p->C;
+    sa.Nf = (int)N;
+    sa.lg = ilog2(N);
+    sa.in_rows = (int)Nu;
+    sa.out_rows = (int)Nu;
+    sa.cc = p->small_cc;
+    sa.lcc = ilog2(p->small_cc);
+    sa.mz = 0xFFFFFFFFu / (uint32_t)(K * p->small_cc) + 1;
+    sa.mv = 0xFFFFFFFFu / (uint32_t)(K * p->small_cc / 2) + 1;
+    sa.groups = (int)((p->C + p->small_cc - 1) / p->small_cc);
+    sa.threads = p->small_threads;
+    sa.bf16 = bf16;
+    e = launch_small(p->L, sa, s);
+    if (e != hipSuccess) goto fail;
+    mark();
+  } else if (p->fused && !mix) {
     // F1 (Y rows w1*64 + n2) -> fused F2 + CG + I1 (V rows w1*64 + n2) -> I2
     const int N1 = (int)p->N1, N2 = 64;
     e = pass(N1, in_pair, OUT_COMPLEX, -1, N2, q, k, p->ws1, Nu * Wz, N * Wz, (int)Wz, 1, N2, 1, N2, 1, 1.0f);
@@ -678,9 +736,38 @@ cgconv_plan_t cgconv_plan_create_boundary(int64_t batch, int64_t N_tokens, int32
   }
   p->n_stages = (p->N1 && !p->fused) ? 5 : 3;
   p->n_stages_mix = p->N1 ? 5 : 3;
+  // DFT length <= 256: the one-block kernel, with the smallest channel group
+  // (a power of two, 2 .. 16) that gives a block at least 256 lanes (two per
+  // point), within the thread and LDS limits
+  const char* no_small = std::getenv("CGCONV_NO_SMALL");
+  if (N <= kSmallMaxNf && L_max <= kSmallLmax && !p->force_generic && !(no_small && no_small[0] == '1')) {
+    const int64_t per_ch = 2 * (N / 2 + 1);  // lanes per channel
+    const int max_threads = small_max_threads(L_max);
+    int cc = 2;
+    while (2 * cc <= 16 && cc < 2 * Cp && per_ch * cc < 256 && per_ch * 2 * cc <= max_threads &&
+           small_lds_bytes(N, K, 2 * cc) <= kSmallMaxLds)
+      cc *= 2;
+    const int64_t threads = (per_ch * cc + 63) / 64 * 64;
+    // a block reads cc of every C channels of a row: with fewer than a
+    // quarter, the loads touch so many more cache lines than they use that
+    // the three kernels, each reading whole rows, are faster (n-body size:
+    // one block 34 us, three kernels 28 us; tiny 10 against 14 us, molecule
+    // size 26 against 27 us)
+    if (threads <= max_threads && small_lds_bytes(N, K, cc) <= kSmallMaxLds && 4 * cc >= C) {
+      p->small = true;
+      p->small_cc = cc;
+      p->small_threads = (int)threads;
+    }
+  }
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) {
     set_error("hipGetDevice failed: %s", hipGetErrorString(e));
+    delete p;
+    return nullptr;
+  }
+  if (p->small && small_lds_bytes(N, K, p->small_cc) > 64 * 1024 &&
+      (e = prepare_small(L_max, (int)small_lds_bytes(N, K, p->small_cc))) != hipSuccess) {
+    set_error("hipFuncSetAttribute failed: %s", hipGetErrorString(e));
     delete p;
     return nullptr;
   }
@@ -1097,6 +1184,7 @@ int cgconv_plan_stage_times(cgconv_plan_t plan, double* ms, int32_t cap, int32_t
     return CGCONV_ERR_INVALID_ARG;
   }
   const int ns = plan->timing_kind == 1 || plan->timing_kind == kKindInter ? plan->n_stages_mix
+                 : plan->timing_kind == kKindSmall ? 1
                  : plan->timing_kind == kKindGate  ? 3
                  : plan->timing_kind == kKindGateBwd ? 4
                  : plan->timing_kind == kKindGraph ? 6
@@ -1130,6 +1218,7 @@ const char* cgconv_plan_stage_name(cgconv_plan_t plan, int32_t stage) {
     if (stage >= plan->n_stages_mix) return "";
     return plan->N1 ? kStagesM2[stage] : kStagesM1[stage];
   }
+  if (plan->timing_kind == kKindSmall) return stage < 1 ? kStagesS[stage] : "";
   if (plan->timing_kind == kKindGate) return stage < 3 ? kStagesG[stage] : "";
   if (plan->timing_kind == kKindGateBwd) return stage < 4 ? kStagesGB[stage] : "";
   if (plan->timing_kind == kKindGraph) return stage < 6 ? kStagesGft[stage] : "";

@@ -167,6 +167,33 @@ struct FusedArgs {
 template <int L>
 hipError_t launch_cg_fused(const FusedArgs& a, hipStream_t s);
 
+// Whole convolution of one batch element and one channel group in one block
+// for DFT lengths Nf <= 256 (see cg_small.hip).  q, k: [B][in_rows][K][C],
+// out: [B][out_rows][K][C] (fp32, or bfloat16 bits when bf16); rows >=
+// in_rows are zero (zero-padded plans).  cc = 2^lcc channels per block (2 ..
+// 16), groups = ceil(C / cc) blocks per batch element, threads >= 2 * (Nf/2
+// + 1) * cc (one lane pair per point).  mz, mv: floor((2^32 - 1) / d) + 1
+// for d = K * cc and K * cc / 2 (divisions by multiply-high).
+struct SmallArgs {
+  const void* q;
+  const void* k;
+  void* out;
+  const float2* tw;  // exp(-2 pi i j / Nf), j < Nf
+  int B, C, Nf, lg, in_rows, out_rows, cc, lcc, groups, threads;
+  uint32_t mz, mv;
+  bool bf16;
+};
+constexpr int kSmallMaxNf = 256;
+constexpr int kSmallMaxLds = 80 * 1024;  // two blocks per CU
+// threads per block: three waves per SIMD up to L_max 4, two (the registers
+// of the L_max 5, 6 lane pairs) above
+constexpr int small_max_threads(int L) { return L <= 4 ? 768 : 512; }
+constexpr int kSmallLmax = 6;
+template <int L>
+hipError_t launch_cg_small(const SmallArgs& a, hipStream_t s);
+template <int L>
+hipError_t prepare_cg_small(int lds_bytes);  // allow lds_bytes of dynamic LDS on the current device
+
 // Highest L_max with a generated, register-resident contraction body.
 int cg_generated_lmax();
 

@@ -101,9 +101,9 @@ def gen_dir(tmp_path_factory):
 
 
 # kernels with DPP moves: the lane-pair contraction (L_max 7; 8 is the same
-# code), the fused kernel's channel-pair stores, the inter-channel kernel and the
-# lane-pair channel-mixing kernel
-UNITS = [("cg_gen.hip", 7), ("cg_fused.hip", 6), ("cg_inter.hip", 4), ("cg_mix.hip", 3)]
+# code), the fused kernel's channel-pair stores, the inter-channel kernel, the
+# lane-pair channel-mixing kernel and the one-block kernel for short token axes
+UNITS = [("cg_gen.hip", 7), ("cg_fused.hip", 6), ("cg_inter.hip", 4), ("cg_mix.hip", 3), ("cg_small.hip", 3)]
 
 
 @pytest.mark.parametrize("unit", UNITS, ids=lambda u: "%s-L%d" % u)

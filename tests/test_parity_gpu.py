@@ -101,6 +101,46 @@ def test_small_workloads_bf16(name):
     assert err <= TOL_BF16
 
 
+@pytest.mark.parametrize("name", SMALL)
+def test_small_workloads_three_kernel_path(name):
+    """The three-kernel single-pass pipeline with the one-block kernel
+    switched off (DFT lengths <= 256 otherwise use it where a block covers
+    at least a quarter of the channels; the backward always uses it)."""
+    q, k = _workload(name)
+    L = W.WORKLOADS[name]["L"]
+    got = gpu_forward(q, k, L, env={"CGCONV_NO_SMALL": "1"}, tag=name + " (three kernels)")
+    ref = cgconv_direct(q, k, L)
+    err = rel_l2(got, ref)
+    print(f"  {name} three kernels: rel_l2 = {err:.3e}", flush=True)
+    assert err <= TOL_F32
+
+
+@pytest.mark.parametrize("shape,stages", [
+    ((1, 64, 2, 4), ["cg_small"]),              # tiny size: all four channels in one block
+    ((32, 32, 4, 32), ["cg_small"]),            # molecule size: eight of 32 channels per block
+    ((1, 2, 0, 1), ["cg_small"]),               # shortest length, one channel
+    ((4, 128, 3, 8), ["cg_small"]),             # two of eight channels per block
+    ((16, 256, 3, 16), ["fft_fwd", "cg", "fft_inv"]),  # n-body size: two of 16 channels per block
+    ((2, 256, 6, 3), ["fft_fwd", "cg", "fft_inv"]),    # spectra beyond the LDS budget
+    ((1, 64, 7, 3), ["fft_fwd", "cg", "fft_inv"]),     # L_max above the one-block kernel's
+], ids=lambda v: "x".join(map(str, v)) if isinstance(v, tuple) else "-".join(v))
+def test_short_length_plans_pick_the_expected_kernels(shape, stages):
+    torch = _torch()
+    import paper_2509_24093_amd as P
+    B, N, L, C = shape
+    K = (L + 1) ** 2
+    print(f"[gpu] stage names B={B} N={N} L={L} C={C}", flush=True)
+    plan = P.Plan(B, N, L, C)
+    q = torch.randn(B, N, K, C, device="cuda")
+    k = torch.randn(B, N, K, C, device="cuda")
+    plan.enable_timing(1)
+    plan(q, k)
+    torch.cuda.synchronize()
+    got, n = plan.stage_times()
+    plan.close()
+    assert n == 1 and list(got) == stages
+
+
 # (B, N, L, C): single-pass lengths 2..256, two-pass 512..65536 (fused up
 # to 32768 at L <= 6, whose outer passes are radix 512 at 32768), every
 # generated L (0..8), odd C and C = 1,
@@ -301,7 +341,8 @@ def test_fused_bf16(shape):
     assert err <= TOL_BF16
 
 
-@pytest.mark.parametrize("N,L,expect", [(256, 3, ["fft_fwd", "cg", "fft_inv"]),
+@pytest.mark.parametrize("N,L,expect", [(256, 3, ["cg_small"]),
+                                        (256, 6, ["fft_fwd", "cg", "fft_inv"]),
                                         (1024, 3, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
                                         (16384, 6, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
                                         (32768, 2, ["fft_fwd_1", "cg_fused", "fft_inv_2"]),
