@@ -118,7 +118,7 @@ __device__ __forceinline__ int radix2_of(int lg) { return lg <= 4 ? 1 : (lg == 5
 struct SmallStore {
   float2* V;    // LDS output tile [row][K][cq], row Nf = trash
   int K, cq, ci;
-  int row;      // bit-reversed destination row of this lane, or Nf
+  int row;      // destination row of this lane (w, N - w), or Nf
   float hsign;
   bool even;
   __device__ __forceinline__ void operator()(int kout, float2 u) const {
