@@ -86,28 +86,39 @@ template <int L>
 struct MixProducer {
   using G = MixGeo<L>;
   char* sm;     // LDS base
-  int off;      // this lane's byte in column (slot 0, point, re) of buffer 0
+  int off;      // this lane's byte in its column of slot 0, buffer 0: the re column
+                // for an even channel, the im column for an odd one, at the
+                // channel pair's first channel
   int half;     // 0: even lane, 1: odd lane of the point
+  bool even;    // even channel of its channel pair (the partner is lane ^ 2)
   float hsign;  // -1 on the odd lane: its value of an odd degree J is -1 times the path value
 
-  // value of slot s of the current step, columns 16 s + 2 pt (re) and + 1
-  // (im), split as v = hi + lo with hi = bf16(v), lo = bf16(v - hi); the odd
-  // lane writes the second path set's slots (S0 on) when the step has one
+  // value of slot s of the current step: columns 16 s + 2 pt (re) and + 1
+  // (im), split as v = hi + lo with hi = bf16(v), lo = bf16(v - hi).  The two
+  // channels of a pair trade halves (one DPP swap): the even channel writes
+  // the pair's re parts, the odd one its im parts, each as one 32-bit hi and
+  // one 32-bit lo word.  With a second path set (S0 > 0) the odd lane writes
+  // the second set's slots (S0 on); otherwise both lanes of a point hold the
+  // same value and split the words, half 0 the hi word and half 1 the lo.
   template <int B, int S0>
   __device__ __forceinline__ void put(int slot, float2 v, bool odd_J) {
     if (odd_J) {
       v.x *= hsign;
       v.y *= hsign;
     }
-    const v2f x = {v.x, v.y};
+    const float r = swap_quad_pair(even ? v.y : v.x);  // partner's re (even channel) or im (odd)
+    const v2f x = even ? v2f{v.x, r} : v2f{r, v.y};    // the pair's re or im parts, channel order
     const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, v2bf));  // one packed conversion
-    const v2f r = {v.x - __uint_as_float(h << 16), v.y - __uint_as_float(h & 0xffff0000u)};
-    const uint32_t l = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, v2bf));
-    char* d = sm + (off + half * (S0 * 16 * 4 * G::RS)) + (B * (4 * G::T_WORDS) + slot * 16 * (4 * G::RS));
-    *reinterpret_cast<uint16_t*>(d) = (uint16_t)h;
-    *reinterpret_cast<uint16_t*>(d + 64) = (uint16_t)l;
-    *reinterpret_cast<uint16_t*>(d + 4 * G::RS) = (uint16_t)(h >> 16);
-    *reinterpret_cast<uint16_t*>(d + 4 * G::RS + 64) = (uint16_t)(l >> 16);
+    const v2f rr = {x.x - __uint_as_float(h << 16), x.y - __uint_as_float(h & 0xffff0000u)};
+    const uint32_t l = __builtin_bit_cast(uint32_t, __builtin_convertvector(rr, v2bf));
+    char* d = sm + off + (B * (4 * G::T_WORDS) + slot * 16 * (4 * G::RS));
+    if constexpr (S0 > 0) {
+      d += half * (S0 * 16 * 4 * G::RS);
+      *reinterpret_cast<uint32_t*>(d) = h;
+      *reinterpret_cast<uint32_t*>(d + 64) = l;
+    } else {
+      *reinterpret_cast<uint32_t*>(d + 64 * half) = half ? l : h;
+    }
   }
 
   // the step's values are staged; the matrix-core waves take them after
@@ -240,7 +251,8 @@ __global__ __launch_bounds__(kMixThreads, 1) void cg_mix_kernel(CgArgs a) {
     load_unpack_half<K, 8>(a, pt, half, x);  // groups of 8: a third of the register file
     MixProducer<L> st;
     st.sm = reinterpret_cast<char*>(smem);
-    st.off = (ptl * 2) * (4 * G::RS) + 2 * c;
+    st.even = (c & 1) == 0;
+    st.off = (ptl * 2 + (c & 1)) * (4 * G::RS) + 2 * (c & ~1);
     st.half = half;
     st.hsign = half ? -1.f : 1.f;
     CgPathSplitBody<L>::produce(x, st);
