@@ -13,9 +13,10 @@
 //
 // Block = one batch element, one head and 4 frequency points w in [0, N/2];
 // lane = (point, pair slot c1*8 + c2), 64 slots per point (m <= 8; a slot
-// with c1 or c2 >= m reads channel h m and meets zero weights).  Each lane
-// forms 2Q of channel h m + c1 and 2K of channel h m + c2 at w from the
-// spectra at w and N - w and evaluates the generated contraction (CgBody).
+// with c1 or c2 >= m meets zero weights).  The block loads the head's
+// spectra at w and N - w of its points into LDS once; each lane forms 2Q of
+// channel h m + c1 and 2K of channel h m + c2 from them and evaluates the
+// generated contraction (CgBody).
 // Every output component is parked in LDS per output phase; after the phase
 // the matrix cores reduce the 64 pair values of each component with the
 // degree's matrix, v_mfma_f32_16x16x4f32 in fp32 (A: rows o padded to 16,
@@ -119,7 +120,11 @@ struct InterStore {
 template <int L>
 __global__ __launch_bounds__(kThreadsI, 2) void cg_inter_kernel(InterArgs a) {
   constexpr int K = InterGeo<L>::K, PMAX = InterGeo<L>::PMAX;
-  __shared__ float2 sT[PMAX * kSlots * kPts];
+  // the spectra of the block's points ([pt][w or N - w][k][channel of the
+  // head], 2 kPts K kInterMmax values) until every lane has gathered its
+  // own, then the parked outputs of the output phases
+  constexpr int ZE = 2 * kPts * K * kInterMmax;
+  __shared__ float2 sT[PMAX * kSlots * kPts > ZE ? PMAX * kSlots * kPts : ZE];
   __shared__ float sW[(L + 1) * 16 * kSlots];
   const int tid = threadIdx.x;
   const int ngroups = (a.F + kPts - 1) / kPts;
@@ -137,52 +142,51 @@ __global__ __launch_bounds__(kThreadsI, 2) void cg_inter_kernel(InterArgs a) {
                   ? a.wt[(((long long)h * (L + 1) + J) * a.mo + o) * a.m * a.m + s1 * a.m + s2]
                   : 0.f;
   }
-  // spectra of query channel h m + c1 and key channel h m + c2 at w and N - w
-  // (points past N/2 and padding slots read a valid row and channel and are
-  // zeroed)
-  const long long wv = w < a.F ? w : 0;
-  const long long wn = (a.N - wv) & (a.N - 1);
   auto rowp = [&](long long x) {
     return ((x & ((1LL << a.n1_log2) - 1)) << a.n2_log2) | (x >> a.n1_log2);
   };
-  const int ch1 = h * a.m + (c1 < a.m ? c1 : 0), ch2 = h * a.m + (c2 < a.m ? c2 : 0);
-  const float2* Zb = a.Z + (long long)b * a.N * K * a.C;
-  const float2* z1a = Zb + rowp(wv) * K * a.C + ch1;
-  const float2* z1b = Zb + rowp(wn) * K * a.C + ch1;
-  const float2* z2a = Zb + rowp(wv) * K * a.C + ch2;
-  const float2* z2b = Zb + rowp(wn) * K * a.C + ch2;
-  float2 qa[K], ka[K];
-  constexpr int G = 4;  // components per load group, one group in flight ahead
-  constexpr int NG = (K + G - 1) / G;
-  float2 buf[2][G][4];
-  auto issue = [&](int gi) {
+  // the head's spectra at w and N - w of the block's points, loaded once
+  // per block (64 contiguous bytes per row and component), four loads per
+  // thread in flight; points past N/2 read row 0, channels past m read zero
+  {
+    const float2* Zb = a.Z + (long long)b * a.N * K * a.C + (long long)h * a.m;
+    constexpr int NB = 4;
+    for (int base = 0; base < ZE; base += NB * kThreadsI) {
+      float2 v[NB];
 #pragma unroll
-    for (int i = 0; i < G; ++i) {
-      const int k = gi * G + i;
-      if (k < K) {
-        const long long off = (long long)k * a.C;
-        buf[gi & 1][i][0] = z1a[off];
-        buf[gi & 1][i][1] = z1b[off];
-        buf[gi & 1][i][2] = z2a[off];
-        buf[gi & 1][i][3] = z2b[off];
+      for (int u = 0; u < NB; ++u) {
+        const int idx = base + u * kThreadsI + tid;
+        const int ch = idx % kInterMmax, k = (idx / kInterMmax) % K, side = (idx / (kInterMmax * K)) & 1,
+                  pl = idx / (2 * kInterMmax * K);
+        const long long wp = (long long)g * kPts + pl;
+        const long long wv = wp < a.F ? wp : 0;
+        const long long row = rowp(side ? (a.N - wv) & (a.N - 1) : wv);
+        v[u] = (idx < ZE && ch < a.m) ? Zb[(row * K + k) * a.C + ch] : make_float2(0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int idx = base + u * kThreadsI + tid;
+        if (idx < ZE) sT[idx] = v[u];
       }
     }
-  };
-  issue(0);
+  }
+  __syncthreads();
+  float2 qa[K], ka[K];
+  {
+    const float2* z1a = sT + ((pt * 2 + 0) * K) * kInterMmax + c1;
+    const float2* z1b = sT + ((pt * 2 + 1) * K) * kInterMmax + c1;
+    const float2* z2a = sT + ((pt * 2 + 0) * K) * kInterMmax + c2;
+    const float2* z2b = sT + ((pt * 2 + 1) * K) * kInterMmax + c2;
 #pragma unroll
-  for (int gi = 0; gi < NG; ++gi) {
-    if (gi + 1 < NG) issue(gi + 1);
-    asm volatile("" ::: "memory");
-#pragma unroll
-    for (int i = 0; i < G; ++i) {
-      const int k = gi * G + i;
-      if (k >= K) break;
-      float2 A1 = buf[gi & 1][i][0], B1 = buf[gi & 1][i][1], A2 = buf[gi & 1][i][2], B2 = buf[gi & 1][i][3];
+    for (int k = 0; k < K; ++k) {
+      const float2 A1 = z1a[k * kInterMmax], B1 = z1b[k * kInterMmax];
+      const float2 A2 = z2a[k * kInterMmax], B2 = z2b[k * kInterMmax];
       qa[k] = valid ? make_float2(A1.x + B1.x, A1.y - B1.y) : make_float2(0.f, 0.f);  // 2Q of channel c1
       ka[k] = valid ? make_float2(A2.y + B2.y, B2.x - A2.x) : make_float2(0.f, 0.f);  // 2K of channel c2
       asm volatile("" : "+v"(qa[k].x), "+v"(qa[k].y), "+v"(ka[k].x), "+v"(ka[k].y));
     }
   }
+  __syncthreads();  // every lane has gathered: the output phases reuse the buffer
   to_complex_basis<K>(qa, ka);
   InterStore<L> st;
   st.T = sT;
