@@ -65,8 +65,15 @@ struct FusedStore {
   const float2* twp;    // LDS: [cls][n2] exp(+2 pi i n2 w1_cls / N)
   const char* Vb;       // V of this batch element (bytes)
   unsigned rowoff0, rowoff1;  // first V row of each class within the batch element
-  int tid, cb, Cp;
+  int wbase, cb, Cp;  // wbase: index of this wave's first thread (uniform)
   bool even, selfpaired;
+
+  // The thread index, rebuilt from the wave's base and the lane id: held in
+  // a vector register across the contraction it would be spilled, and the
+  // reload's wait on the memory counter would also wait for the V stores.
+  __device__ __forceinline__ int tid() const {
+    return wbase + (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  }
 
   // output component kout = J^2 + J + M of phase mu = |M|, slot ci within
   // the phase: J for mu = 0, 2 (J - mu) + (M < 0) otherwise
@@ -89,7 +96,7 @@ struct FusedStore {
     const int nc = mu == 0 ? L + 1 : 2 * (L + 1 - mu);
     const int ncol = 2 * nc * 2;  // (cls, ci, pair)
     __syncthreads();              // every lane has parked its outputs
-    for (int it = tid; it < ncol * 8; it += kThreadsF) {
+    for (int it = tid(); it < ncol * 8; it += kThreadsF) {
       const int col = it % ncol, j1 = it / ncol;
       const int pair = col & 1, ci = (col >> 1) % nc, cls = (col >> 1) / nc;
       const float2* src = O1 + ((cls * kN2 + j1) * PMAX + ci) * 2 + pair;
@@ -102,7 +109,7 @@ struct FusedStore {
       for (int s = 0; s < 8; ++s) dst[s * PMAX * 2] = x[s];
     }
     __syncthreads();
-    for (int it = tid; it < ncol * 8; it += kThreadsF) {
+    for (int it = tid(); it < ncol * 8; it += kThreadsF) {
       const int col = it % ncol, j2 = it / ncol;
       const int pair = col & 1, ci = (col >> 1) % nc, cls = (col >> 1) / nc;
       const float2* src = O2 + ((cls * kN2 + j2) * PMAX + ci) * 2 + pair;
@@ -295,7 +302,7 @@ __global__ __launch_bounds__(kThreadsF, 2) void cg_fused_kernel(FusedArgs a) {
   st.Vb = reinterpret_cast<const char*>(a.V + (long long)b * N * K * a.Cp);
   st.rowoff0 = (unsigned)(w1 * kN2);
   st.rowoff1 = (unsigned)(w1b * kN2);
-  st.tid = tid;
+  st.wbase = __builtin_amdgcn_readfirstlane(tid & ~63);
   st.cb = cb;
   st.Cp = a.Cp;
   st.even = (cc & 1) == 0;
