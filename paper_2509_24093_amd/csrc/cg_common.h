@@ -34,6 +34,15 @@ __device__ __forceinline__ float swap_pair(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
 }
 
+// The key operand of one block (m1, m2) of the generated contraction: the
+// array itself; a kernel that reads the key spectra from LDS overloads this
+// to hand each block a fresh view, so that the block's loads are not merged
+// with another block's and no key value stays in a register past its block.
+template <class T>
+__device__ __forceinline__ const T& cg_kfence(const T& k) {
+  return k;
+}
+
 // value of the lane with index lane ^ 1 (a lane-swap move; the lane-pair
 // contraction keeps every lane active).  Written as volatile assembly so
 // that it stays where the generated code puts it, next to the products that

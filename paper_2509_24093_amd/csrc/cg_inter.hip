@@ -14,9 +14,13 @@
 // Block = one batch element, one head and 4 frequency points w in [0, N/2];
 // lane = (point, pair slot c1*8 + c2), 64 slots per point (m <= 8; a slot
 // with c1 or c2 >= m meets zero weights).  The block loads the head's
-// spectra at w and N - w of its points into LDS once; each lane forms 2Q of
-// channel h m + c1 and 2K of channel h m + c2 from them and evaluates the
-// generated contraction (CgBody).
+// spectra at w and N - w of its points into LDS once.  Each lane forms 2Q of
+// channel h m + c1 in registers; 2K of every key channel is formed once per
+// point, in the complex-m basis, and stays in LDS, where the eight lanes of a
+// key channel read it (broadcast) block by block of the generated
+// contraction (CgBody with an LDS key operand).  With the key operand out of
+// the registers a lane needs 166 VGPRs instead of 256, so three waves share
+// a SIMD instead of two.
 // Every output component is parked in LDS per output phase; after the phase
 // the matrix cores reduce the 64 pair values of each component with the
 // degree's matrix, v_mfma_f32_16x16x4f32 in fp32 (A: rows o padded to 16,
@@ -42,6 +46,28 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 constexpr int kPts = 4;      // frequency points per block
 constexpr int kSlots = 64;   // channel-pair slots per point
 constexpr int kThreadsI = kPts * kSlots;
+constexpr int kWRows = kInterMmax;  // rows o of the reduction matrices held in LDS (m_out <= m)
+
+// The key spectra of the block's points in LDS ([pt][k][c2], complex-m
+// basis): the lanes of a point share them, eight lanes per key channel, and
+// the eight key channels of a component are 64 contiguous bytes.
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) const v2f lds_cf2;
+struct LdsKey {
+  lds_cf2* p;  // this lane's key channel at component 0
+  __device__ __forceinline__ float2 operator[](int k) const {
+    const v2f v = p[k * kInterMmax];
+    return make_float2(v.x, v.y);
+  }
+};
+// A fresh, opaque copy per block of the contraction: the block's loads are
+// not merged with another block's, so no key value stays live in a register
+// beyond its block.
+__device__ __forceinline__ LdsKey cg_kfence(const LdsKey& k) {
+  LdsKey r = k;
+  asm volatile("" : "+v"(r.p));
+  return r;
+}
 
 template <int L>
 struct InterGeo {
@@ -54,7 +80,7 @@ struct InterStore {
   static constexpr int PMAX = InterGeo<L>::PMAX;
   static constexpr int K = InterGeo<L>::K;
   float2* T;        // LDS [PMAX][kSlots][kPts]: parked outputs of the current phase
-  const float* Wl;  // LDS [L+1][16][kSlots]: the head's matrices, rows o padded to 16
+  const float* Wl;  // LDS [L+1][kWRows][kSlots]: the head's matrices (rows o >= kWRows of the MFMA operand are zero)
   char* Wb;         // packed output spectra of this batch element (bytes)
   long long N;
   int n1_log2, n2_log2, F, w0, Cpo, co0, mo;
@@ -86,7 +112,7 @@ struct InterStore {
 #pragma unroll
       for (int step = 0; step < kSlots / 4; ++step) {
         const int k = 4 * step + kq;
-        const float av = Wl[(J * 16 + col) * kSlots + k];  // A[o = col][pair k]
+        const float av = col < kWRows ? Wl[(J * kWRows + col) * kSlots + k] : 0.f;  // A[o = col][pair k]
         const float2 t = T[(ci * kSlots + k) * kPts + cpt];
         const float bv = has ? (ri ? t.y : t.x) : 0.f;    // B[pair k][col]
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
@@ -118,14 +144,15 @@ struct InterStore {
 };
 
 template <int L>
-__global__ __launch_bounds__(kThreadsI, 2) void cg_inter_kernel(InterArgs a) {
+__global__ __launch_bounds__(kThreadsI, 3) void cg_inter_kernel(InterArgs a) {
   constexpr int K = InterGeo<L>::K, PMAX = InterGeo<L>::PMAX;
   // the spectra of the block's points ([pt][w or N - w][k][channel of the
   // head], 2 kPts K kInterMmax values) until every lane has gathered its
   // own, then the parked outputs of the output phases
   constexpr int ZE = 2 * kPts * K * kInterMmax;
   __shared__ float2 sT[PMAX * kSlots * kPts > ZE ? PMAX * kSlots * kPts : ZE];
-  __shared__ float sW[(L + 1) * 16 * kSlots];
+  __shared__ float sW[(L + 1) * kWRows * kSlots];
+  __shared__ float2 sK[kPts * K * kInterMmax];
   const int tid = threadIdx.x;
   const int ngroups = (a.F + kPts - 1) / kPts;
   const int g = blockIdx.x % ngroups, bh = blockIdx.x / ngroups;
@@ -135,8 +162,8 @@ __global__ __launch_bounds__(kThreadsI, 2) void cg_inter_kernel(InterArgs a) {
   const long long w = (long long)g * kPts + pt;
   const bool valid = w < a.F && c1 < a.m && c2 < a.m;
   // the head's matrices, rows o < mo and slots of real pairs, zeros elsewhere
-  for (int idx = tid; idx < (L + 1) * 16 * kSlots; idx += kThreadsI) {
-    const int J = idx / (16 * kSlots), o = (idx / kSlots) % 16, s = idx % kSlots;
+  for (int idx = tid; idx < (L + 1) * kWRows * kSlots; idx += kThreadsI) {
+    const int J = idx / (kWRows * kSlots), o = (idx / kSlots) % kWRows, s = idx % kSlots;
     const int s1 = s >> 3, s2 = s & 7;
     sW[idx] = (o < a.mo && s1 < a.m && s2 < a.m)
                   ? a.wt[(((long long)h * (L + 1) + J) * a.mo + o) * a.m * a.m + s1 * a.m + s2]
@@ -171,23 +198,49 @@ __global__ __launch_bounds__(kThreadsI, 2) void cg_inter_kernel(InterArgs a) {
     }
   }
   __syncthreads();
-  float2 qa[K], ka[K];
+  // 2K of every key channel of the block's points, in the complex-m basis,
+  // into sK; each lane's 2Q into registers
+  for (int idx = tid; idx < kPts * K * kInterMmax; idx += kThreadsI) {
+    const int ch = idx % kInterMmax, k = (idx / kInterMmax) % K, pl = idx / (kInterMmax * K);
+    const int l = (int)__builtin_sqrtf((float)k + 0.5f), m = k - l * l - l;
+    auto key2 = [&](int kk) {
+      const float2 A = sT[((pl * 2 + 0) * K + kk) * kInterMmax + ch], B = sT[((pl * 2 + 1) * K + kk) * kInterMmax + ch];
+      return make_float2(A.y + B.y, B.x - A.x);
+    };
+    float2 v;
+    if (m == 0) {
+      v = key2(k);
+    } else {
+      const int mu = m < 0 ? -m : m;
+      const float2 xc = key2(l * l + l + mu), xs = key2(l * l + l - mu);
+      v = m < 0 ? make_float2(xc.x - xs.y, xc.y + xs.x) : make_float2(xc.x + xs.y, xc.y - xs.x);
+    }
+    const bool kv = (long long)g * kPts + pl < a.F && ch < a.m;
+    sK[idx] = kv ? v : make_float2(0.f, 0.f);
+  }
+  float2 qa[K];
   {
     const float2* z1a = sT + ((pt * 2 + 0) * K) * kInterMmax + c1;
     const float2* z1b = sT + ((pt * 2 + 1) * K) * kInterMmax + c1;
-    const float2* z2a = sT + ((pt * 2 + 0) * K) * kInterMmax + c2;
-    const float2* z2b = sT + ((pt * 2 + 1) * K) * kInterMmax + c2;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       const float2 A1 = z1a[k * kInterMmax], B1 = z1b[k * kInterMmax];
-      const float2 A2 = z2a[k * kInterMmax], B2 = z2b[k * kInterMmax];
       qa[k] = valid ? make_float2(A1.x + B1.x, A1.y - B1.y) : make_float2(0.f, 0.f);  // 2Q of channel c1
-      ka[k] = valid ? make_float2(A2.y + B2.y, B2.x - A2.x) : make_float2(0.f, 0.f);  // 2K of channel c2
-      asm volatile("" : "+v"(qa[k].x), "+v"(qa[k].y), "+v"(ka[k].x), "+v"(ka[k].y));
+      asm volatile("" : "+v"(qa[k].x), "+v"(qa[k].y));
     }
   }
-  __syncthreads();  // every lane has gathered: the output phases reuse the buffer
-  to_complex_basis<K>(qa, ka);
+  __syncthreads();  // every lane has gathered and sK is complete: the output phases reuse sT
+#pragma unroll
+  for (int l = 1; l * l < K; ++l) {
+#pragma unroll
+    for (int mu = 1; mu <= l; ++mu) {
+      const int c = l * l + l + mu, s = l * l + l - mu;
+      const float2 xc = qa[c], xs = qa[s];
+      qa[s] = make_float2(xc.x - xs.y, xc.y + xs.x);
+      qa[c] = make_float2(xc.x + xs.y, xc.y - xs.x);
+    }
+  }
+  const LdsKey ka{(lds_cf2*)(sK + pt * K * kInterMmax + c2)};
   InterStore<L> st;
   st.T = sT;
   st.Wl = sW;
@@ -211,7 +264,7 @@ __global__ __launch_bounds__(kThreadsI, 2) void cg_inter_kernel(InterArgs a) {
 
 template <>
 hipError_t launch_cg_inter<CGCONV_TU_L>(const InterArgs& a, hipStream_t s) {
-  if (a.m < 1 || a.m > kInterMmax || a.mo < 2 || a.mo > 16 || (a.mo & 1) || a.C != a.H * a.m || a.F < 1)
+  if (a.m < 1 || a.m > kInterMmax || a.mo < 2 || a.mo > kWRows || (a.mo & 1) || a.C != a.H * a.m || a.F < 1)
     return hipErrorInvalidValue;
   const long long blocks = (long long)a.B * a.H * ((a.F + kPts - 1) / kPts);
   hipLaunchKernelGGL(cg_inter_kernel<CGCONV_TU_L>, dim3((unsigned)blocks), dim3(kThreadsI), 0, s, a);

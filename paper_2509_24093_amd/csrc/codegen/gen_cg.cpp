@@ -113,7 +113,7 @@ struct Emitter {
 using TermMap = std::map<std::array<int, 4>, std::vector<Term>>;  // (l1, m1, l2, m2) -> terms
 
 std::string qname(int l, int m) { return "qa[" + std::to_string(comp(l, m)) + "]"; }
-std::string kname(int l, int m) { return "ka[" + std::to_string(comp(l, m)) + "]"; }
+std::string kname(int l, int m) { return "kb[" + std::to_string(comp(l, m)) + "]"; }
 
 // Cheaper of product and key form for one half (fixed factor f1 of the l1
 // side, varying factor of the l2 side) with the given (l2 -> terms) lists.
@@ -281,11 +281,11 @@ void emit_body(FILE* f, int L, long* ops_out) {
 
   Emitter e{f, {}, 0};
   std::fprintf(f, "template <>\nstruct CgBody<%d> {\n  static constexpr int K = %d;\n", L, K);
-  std::fprintf(f, "  template <class Store>\n");
-  std::fprintf(f,
-               "  static __device__ __forceinline__ void run(const float2 (&qa)[%d], const float2 (&ka)[%d], "
-               "Store& st) {\n",
-               K, K);
+  // ka: an array of K float2, or an accessor whose operator[] returns the
+  // component by value (a kernel whose lanes share key spectra reads them
+  // from LDS)
+  std::fprintf(f, "  template <class Store, class KA>\n");
+  std::fprintf(f, "  static __device__ __forceinline__ void run(const float2 (&qa)[%d], const KA& ka, Store& st) {\n", K);
   for (int mu = 0; mu <= L; ++mu) {
     std::fprintf(f, "    {  // phase |M| = %d\n", mu);
     std::vector<int> Ms = mu == 0 ? std::vector<int>{0} : std::vector<int>{mu, -mu};
@@ -296,7 +296,9 @@ void emit_body(FILE* f, int L, long* ops_out) {
         const int m2 = M - m1;
         if (m2 < -L || m2 > L || m1 > m2) continue;
         std::fprintf(f, "      // blocks m1=%d m2=%d and swapped\n", m1, m2);
+        std::fprintf(f, "      {\n      const auto& kb = cg_kfence(ka);\n");
         for (int l1 = std::abs(m1); l1 <= L; ++l1) emit_row(e, terms_of, M, l1, m1, m2);
+        std::fprintf(f, "      }\n");
       }
     }
     // output transform and stores
