@@ -1,7 +1,8 @@
 """Inter-channel CG convolution with the per-degree reduction
 (cgconv_forward_interchannel) against the oracle, through the C ABI: every
 forward pass configuration (single pass, unfused two-pass), L_max 0..6,
-several head and channel counts (m = 1..8, odd m), m_out < m and = m, the
+several head and channel counts (m = 1..8, odd m), m_out < m and = m, one
+whole batch element at the point-cloud token length, the
 linear boundary, a selector map against the plain convolution, argument
 errors."""
 
@@ -117,3 +118,17 @@ def test_interchannel_argument_errors():
             P.CGCONV_ERR_UNSUPPORTED  # L_max 7
     finally:
         plan.close()
+
+
+def test_interchannel_full_length_whole_batch_element():
+    """The point-cloud token length and head width (N = 16384, L_max 6, a
+    head of 8 channels, every pair reduced to 8): batch element 1 of two
+    compared whole (all tokens, components and output channels) against the
+    oracle's FFT mode."""
+    B, N, L, H, m, mo = 2, 16384, 6, 1, 8, 8
+    print(f"[gpu] interchannel full length {(B, N, L, H, m, mo)}", flush=True)
+    q, k, wt, got = _run(B, N, L, H, m, mo, seed=2031)
+    ref = cgconv_interchannel(q[1:2], k[1:2], L, heads=H, W=wt, mode="fft")
+    err = rel_l2(got[1:2], ref)
+    print(f"  rel_l2 = {err:.3e}", flush=True)
+    assert err <= TOL_F32
