@@ -40,7 +40,6 @@ namespace {
 
 using cgdev::CgBody;
 using cgdev::swap_pair;
-using cgdev::to_complex_basis;
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int kPts = 4;      // frequency points per block
@@ -230,6 +229,7 @@ __global__ __launch_bounds__(kThreadsI, 3) void cg_inter_kernel(InterArgs a) {
     }
   }
   __syncthreads();  // every lane has gathered and sK is complete: the output phases reuse sT
+  // 2Q into the complex-m basis (the basis change of the other kernels, on one operand)
 #pragma unroll
   for (int l = 1; l * l < K; ++l) {
 #pragma unroll
